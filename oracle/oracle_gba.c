@@ -1,0 +1,207 @@
+/*
+ * oracle_gba.c -- CPU reference for the fused matmul + bias + ReLU.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path links, loads or
+ * calls this file: only the tests, the smoke check and the benchmark's CPU
+ * baseline leg do.  It shares no code, header or constant with the HIP
+ * library.
+ *
+ * What it computes (Problem Statement section, Listing 1 and the expression
+ * tree described there: the root of the pointwise statement is ReLU, its
+ * child is the add of the matmul result and the bias):
+ *
+ *     pre(i,j) = sum_{k=0..K-1} A(i,k) * B(k,j)  +  bias(j)
+ *     out(i,j) = act == RELU ? (pre > 0 ? pre : 0) : pre
+ *
+ * evaluated in IEEE binary64 with k ascending, the bias added last, and no
+ * rounding to fp16 anywhere.  Inputs are fp16 bit patterns decoded by the
+ * routine below (sign, 5-bit exponent, 10-bit fraction, subnormals).  The
+ * product of two fp16 values is exact in binary64 (11 + 11 significant bits),
+ * so the only rounding is in the running sum.
+ *
+ * Operand storage (row- or column-major A and B, Background section and the
+ * four layout specialisations of the Matmul Compute Decomposition section):
+ *     A(i,k) = layout_a == ROW ? A[i*lda + k] : A[k*lda + i]
+ *     B(k,j) = layout_b == ROW ? B[k*ldb + j] : B[j*ldb + k]
+ * The output is written row-major as doubles: out[r*ldo + j].
+ *
+ * Readings of points the paper leaves open: bias is a length-N vector
+ * broadcast over rows (NULL = no bias); leading dimensions have BLAS meaning.
+ *
+ * Build: plain C11, no -ffast-math, -ffp-contract=off (no fused multiply-add,
+ * so every product is rounded exactly as written).
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { OR_ROW = 0, OR_COL = 1 };
+enum { OR_ACT_NONE = 0, OR_ACT_RELU = 1 };
+
+/* IEEE 754 binary16 -> binary64, written out from the format definition. */
+double oracle_f16_to_f64(uint16_t h)
+{
+    int sign = (h >> 15) & 1;
+    int expo = (h >> 10) & 0x1f;
+    int frac = h & 0x3ff;
+    double v;
+    if (expo == 0)              /* zero or subnormal: frac * 2^-24 */
+        v = ldexp((double)frac, -24);
+    else if (expo == 31)        /* infinity or NaN */
+        v = frac ? NAN : INFINITY;
+    else                        /* normal: (1 + frac/1024) * 2^(expo-15) */
+        v = ldexp((double)(1024 + frac), expo - 25);
+    return sign ? -v : v;
+}
+
+typedef struct {
+    int layout_a;
+    int64_t M, N, K;
+    const uint16_t *A;
+    int64_t lda;
+    const double *Bd;        /* decoded logical B, K x N row-major */
+    const double *biasd;     /* decoded bias or NULL */
+    int act;
+    const int64_t *rows;     /* rows to evaluate (NULL = 0..M-1) */
+    int64_t nrows;
+    double *out;
+    int64_t ldo;
+    int nthreads, tid;
+} job_t;
+
+static double a_elem(const job_t *J, int64_t i, int64_t k)
+{
+    uint16_t h = J->layout_a == OR_ROW ? J->A[i * J->lda + k] : J->A[k * J->lda + i];
+    return oracle_f16_to_f64(h);
+}
+
+/* One output row: the i-k-j loop, k ascending, then bias, then activation. */
+static void row_worker(const job_t *J, int64_t r, double *acc)
+{
+    int64_t i = J->rows ? J->rows[r] : r;
+    for (int64_t j = 0; j < J->N; ++j)
+        acc[j] = 0.0;
+    for (int64_t k = 0; k < J->K; ++k) {
+        double a = a_elem(J, i, k);
+        const double *brow = J->Bd + k * J->N;
+        for (int64_t j = 0; j < J->N; ++j)
+            acc[j] = acc[j] + a * brow[j];
+    }
+    double *o = J->out + r * J->ldo;
+    for (int64_t j = 0; j < J->N; ++j) {
+        double pre = acc[j] + (J->biasd ? J->biasd[j] : 0.0);
+        o[j] = (J->act == OR_ACT_RELU) ? (pre > 0.0 ? pre : 0.0) : pre;
+    }
+}
+
+static void *thread_main(void *arg)
+{
+    job_t *J = (job_t *)arg;
+    double *acc = (double *)malloc((size_t)(J->N > 0 ? J->N : 1) * sizeof(double));
+    if (!acc)
+        return (void *)1;
+    for (int64_t r = J->tid; r < J->nrows; r += J->nthreads)
+        row_worker(J, r, acc);
+    free(acc);
+    return NULL;
+}
+
+/*
+ * Evaluate out for the listed rows (rows == NULL: every row 0..M-1, nrows
+ * must equal M).  out has nrows rows of stride ldo.  Returns 0 on success,
+ * 1 on bad arguments, 2 on allocation or thread failure.
+ */
+int oracle_gemm_bias_act_rows_f64(int layout_a, int layout_b,
+                                  int64_t M, int64_t N, int64_t K,
+                                  const uint16_t *A, int64_t lda,
+                                  const uint16_t *B, int64_t ldb,
+                                  const uint16_t *bias, int act,
+                                  const int64_t *rows, int64_t nrows,
+                                  double *out, int64_t ldo, int nthreads)
+{
+    if (M < 0 || N < 0 || K < 0 || nrows < 0 || ldo < N)
+        return 1;
+    if ((layout_a != OR_ROW && layout_a != OR_COL) || (layout_b != OR_ROW && layout_b != OR_COL))
+        return 1;
+    if (act != OR_ACT_NONE && act != OR_ACT_RELU)
+        return 1;
+    if (M > 0 && K > 0 && lda < (layout_a == OR_ROW ? K : M))
+        return 1;
+    if (N > 0 && K > 0 && ldb < (layout_b == OR_ROW ? N : K))
+        return 1;
+    if (!rows && nrows != M)
+        return 1;
+    for (int64_t r = 0; rows && r < nrows; ++r)
+        if (rows[r] < 0 || rows[r] >= M)
+            return 1;
+    if (nrows == 0 || N == 0)
+        return 0;
+    if (nthreads < 1)
+        nthreads = 1;
+
+    /* fp64 copy of the logical K x N matrix B, and of the bias. */
+    double *Bd = (double *)malloc((size_t)(K > 0 ? K : 1) * (size_t)N * sizeof(double));
+    double *biasd = bias ? (double *)malloc((size_t)N * sizeof(double)) : NULL;
+    if (!Bd || (bias && !biasd)) {
+        free(Bd);
+        free(biasd);
+        return 2;
+    }
+    for (int64_t k = 0; k < K; ++k)
+        for (int64_t j = 0; j < N; ++j) {
+            uint16_t h = layout_b == OR_ROW ? B[k * ldb + j] : B[j * ldb + k];
+            Bd[k * N + j] = oracle_f16_to_f64(h);
+        }
+    for (int64_t j = 0; bias && j < N; ++j)
+        biasd[j] = oracle_f16_to_f64(bias[j]);
+
+    if (nthreads > nrows)
+        nthreads = (int)nrows;
+    job_t *jobs = (job_t *)calloc((size_t)nthreads, sizeof(job_t));
+    pthread_t *th = (pthread_t *)calloc((size_t)nthreads, sizeof(pthread_t));
+    int rc = 0;
+    if (!jobs || !th) {
+        rc = 2;
+        goto done;
+    }
+    for (int t = 0; t < nthreads; ++t) {
+        job_t J = {layout_a, M, N, K, A, lda, Bd, biasd, act, rows, nrows, out, ldo, nthreads, t};
+        jobs[t] = J;
+    }
+    int started = 0;
+    for (int t = 1; t < nthreads; ++t) {
+        if (pthread_create(&th[t], NULL, thread_main, &jobs[t]) != 0) {
+            rc = 2;
+            break;
+        }
+        started = t;
+    }
+    if (thread_main(&jobs[0]) != NULL)
+        rc = 2;
+    for (int t = 1; t <= started; ++t) {
+        void *ret = NULL;
+        pthread_join(th[t], &ret);
+        if (ret != NULL)
+            rc = 2;
+    }
+done:
+    free(jobs);
+    free(th);
+    free(Bd);
+    free(biasd);
+    return rc;
+}
+
+/* Every row: out is M x N with stride ldo. */
+int oracle_gemm_bias_act_f64(int layout_a, int layout_b,
+                             int64_t M, int64_t N, int64_t K,
+                             const uint16_t *A, int64_t lda,
+                             const uint16_t *B, int64_t ldb,
+                             const uint16_t *bias, int act,
+                             double *out, int64_t ldo, int nthreads)
+{
+    return oracle_gemm_bias_act_rows_f64(layout_a, layout_b, M, N, K, A, lda, B, ldb, bias, act,
+                                         NULL, M, out, ldo, nthreads);
+}

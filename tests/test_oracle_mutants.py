@@ -1,0 +1,68 @@
+"""Strength of the oracle's pins: copies of the oracle with one planted
+mistake each (built on the CPU, never used anywhere else) must each fail at
+least one pin.  The real oracle source is read, not modified."""
+import os
+import subprocess
+
+import pytest
+
+from oracle import build_oracle
+from oracle import oracle as O
+import oracle_pins as P
+
+# (name, text in oracle_gba.c, replacement) -- each a plausible slip.
+MUTANTS = [
+    ("sign_of_product", "acc[j] = acc[j] + a * brow[j];", "acc[j] = acc[j] - a * brow[j];"),
+    ("dropped_bias", "(J->biasd ? J->biasd[j] : 0.0)", "0.0"),
+    ("relu_before_bias", "double pre = acc[j] + (J->biasd ? J->biasd[j] : 0.0);\n"
+     "        o[j] = (J->act == OR_ACT_RELU) ? (pre > 0.0 ? pre : 0.0) : pre;",
+     "double r = (J->act == OR_ACT_RELU) ? (acc[j] > 0.0 ? acc[j] : 0.0) : acc[j];\n"
+     "        o[j] = r + (J->biasd ? J->biasd[j] : 0.0);"),
+    ("a_transposed", "J->layout_a == OR_ROW ? J->A[i * J->lda + k]",
+     "J->layout_a == OR_COL ? J->A[i * J->lda + k]"),
+    ("b_transposed", "layout_b == OR_ROW ? B[k * ldb + j]", "layout_b == OR_COL ? B[k * ldb + j]"),
+    ("last_k_dropped", "for (int64_t k = 0; k < J->K; ++k) {", "for (int64_t k = 0; k + 1 < J->K; ++k) {"),
+    ("first_k_dropped", "for (int64_t k = 0; k < J->K; ++k) {", "for (int64_t k = 1; k < J->K; ++k) {"),
+    ("exponent_bias", "expo - 25", "expo - 24"),
+    ("subnormal_scale", "ldexp((double)frac, -24)", "ldexp((double)frac, -25)"),
+    ("implicit_bit", "(double)(1024 + frac)", "(double)(frac)"),
+    ("relu_leaky", "(pre > 0.0 ? pre : 0.0)", "(pre > 0.0 ? pre : 0.01 * pre)"),
+    ("relu_clamps_small", "(pre > 0.0 ? pre : 0.0)", "(pre > 0.5 ? pre : 0.0)"),
+    ("relu_inverted", "J->act == OR_ACT_RELU", "J->act == OR_ACT_NONE"),
+    ("lda_ignored", "J->A[i * J->lda + k] : J->A[k * J->lda + i]",
+     "J->A[i * J->K + k] : J->A[k * J->M + i]"),
+    ("ldb_ignored", "B[k * ldb + j] : B[j * ldb + k]", "B[k * N + j] : B[j * K + k]"),
+    ("bias_index_by_row", "J->biasd ? J->biasd[j] : 0.0", "J->biasd ? J->biasd[i % J->N] : 0.0"),
+    ("b_row_index", "const double *brow = J->Bd + k * J->N;",
+     "const double *brow = J->Bd + (J->K - 1 - k) * J->N;"),
+]
+
+
+def _build_mutant(tmp_path, name, old, new):
+    src = open(build_oracle.SRC).read()
+    assert src.count(old) >= 1, f"mutation anchor for {name} not found"
+    mutated = src.replace(old, new, 1)
+    c = tmp_path / f"mut_{name}.c"
+    so = tmp_path / f"libmut_{name}.so"
+    c.write_text(mutated)
+    subprocess.run(["gcc", "-std=c11", "-O2", "-ffp-contract=off", "-fPIC", "-shared", "-w",
+                    "-o", str(so), str(c), "-lm", "-lpthread"], check=True)
+    return O.load_library(str(so))
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, name, old, new):
+    lib = _build_mutant(tmp_path, name, old, new)
+    failed = []
+    for pin in P.PINS:
+        try:
+            pin(lib)
+        except (AssertionError, ValueError):
+            failed.append(pin.__name__)
+    assert failed, f"mutant {name} passed every pin"
+
+
+def test_unmutated_copy_passes(tmp_path):
+    lib = _build_mutant(tmp_path, "none", "#include <math.h>", "#include <math.h>")
+    for pin in P.PINS:
+        pin(lib)
