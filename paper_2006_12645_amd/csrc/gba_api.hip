@@ -1,0 +1,253 @@
+// gba_api.hip -- the C entry points of libgba.so: argument validation, tile
+// selection, launch on the caller's stream, and the unfused baseline's
+// pointwise kernels.  Declarations and contracts are in include/gba.h.
+#include <limits.h>
+#include <stdint.h>
+
+#include "gba.h"
+#include "gba_tiles.hpp"
+
+namespace gba {
+namespace {
+
+bool is_layout(int v) { return v == GBA_ROW_MAJOR || v == GBA_COL_MAJOR; }
+
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+gba_status validate_gemm(int la, int lb, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
+                         const void *B, int64_t ldb, const void *bias, const void *C, int64_t ldc,
+                         int act, int accum)
+{
+    if (!is_layout(la) || !is_layout(lb)) return GBA_EINVAL;
+    if (act != GBA_ACT_NONE && act != GBA_ACT_RELU) return GBA_EINVAL;
+    if (accum != GBA_ACC_F32 && accum != GBA_ACC_F16) return GBA_EINVAL;
+    if (M < 0 || N < 0 || K < 0 || lda < 0 || ldb < 0 || ldc < 0) return GBA_EINVAL;
+    if (M > INT_MAX || N > INT_MAX || K > INT_MAX) return GBA_EUNSUPPORTED;
+    if (M == 0 || N == 0) return GBA_OK;
+    if (C == nullptr || ldc < N) return GBA_EINVAL;
+    if (K > 0) {
+        if (A == nullptr || B == nullptr) return GBA_EINVAL;
+        if (lda < (la == GBA_ROW_MAJOR ? K : M)) return GBA_EINVAL;
+        if (ldb < (lb == GBA_ROW_MAJOR ? N : K)) return GBA_EINVAL;
+    }
+    if (!aligned(A, 2) || !aligned(B, 2) || !aligned(C, 2) || !aligned(bias, 2))
+        return GBA_EUNSUPPORTED;
+    return GBA_OK;
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Tile choice by problem shape: the largest block tile that still yields
+// enough workgroups to occupy the 256 compute units.
+int select_tile(int64_t M, int64_t N, int64_t K)
+{
+    (void)K;
+    const int64_t CUS = 256;
+    if (ceil_div(M, 256) * ceil_div(N, 256) >= CUS) return 0;
+    if (ceil_div(M, 256) * ceil_div(N, 128) >= CUS) return 3;
+    if (ceil_div(M, 128) * ceil_div(N, 128) >= CUS) return 2;
+    if (ceil_div(M, 64) * ceil_div(N, 128) >= CUS) return 7;
+    if (M <= 32) return 6;
+    return 5;
+}
+
+const LayoutTable &table_for(int la, int lb)
+{
+    if (la == GBA_ROW_MAJOR) return lb == GBA_ROW_MAJOR ? table_RR() : table_RC();
+    return lb == GBA_ROW_MAJOR ? table_CR() : table_CC();
+}
+
+gba_status run_gemm(int la, int lb, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
+                    const void *B, int64_t ldb, const void *bias, void *C, int64_t ldc, int act,
+                    int accum, int tile_id, hipStream_t stream)
+{
+    if (tile_id >= NUM_TILES) return GBA_EINVAL;
+    gba_status st = validate_gemm(la, lb, M, N, K, A, lda, B, ldb, bias, C, ldc, act, accum);
+    if (st != GBA_OK || M == 0 || N == 0) return st;
+
+    const bool vec = aligned(A, 16) && aligned(B, 16) && aligned(C, 16) && aligned(bias, 16) &&
+                     lda % 8 == 0 && ldb % 8 == 0 && ldc % 8 == 0;
+    const int tile = !vec ? GENERIC_TILE : (tile_id >= 0 ? tile_id : select_tile(M, N, K));
+    const TileCfg &cfg = TILES[tile];
+
+    GemmArgs a;
+    a.A = static_cast<const _Float16 *>(A);
+    a.B = static_cast<const _Float16 *>(B);
+    a.bias = static_cast<const _Float16 *>(bias);
+    a.C = static_cast<_Float16 *>(C);
+    a.lda = lda;
+    a.ldb = ldb;
+    a.ldc = ldc;
+    a.M = (int)M;
+    a.N = (int)N;
+    a.K = (int)K;
+    a.relu = act == GBA_ACT_RELU;
+    a.tiles_m = (int)ceil_div(M, cfg.bm);
+    a.tiles_n = (int)ceil_div(N, cfg.bn);
+    if ((int64_t)a.tiles_m * a.tiles_n > INT_MAX) return GBA_EUNSUPPORTED;
+
+    const LayoutTable &tab = table_for(la, lb);
+    const int acc16 = accum == GBA_ACC_F16;
+    LaunchFn fn = vec ? tab.vec[tile][acc16] : tab.scalar[acc16];
+    return fn(a, stream) == hipSuccess ? GBA_OK : GBA_EHIP;
+}
+
+// ---------------------------------------------------------------------------
+// Unfused baseline: in-place bias add and ReLU over a row-major fp16 matrix.
+// HBM-bound; each thread handles 16-byte chunks of a row.
+
+template <bool VEC>
+__global__ void __launch_bounds__(256) bias_add_kernel(_Float16 *C, int64_t ldc, const _Float16 *bias,
+                                                       int M, int N)
+{
+    const int64_t nch = (N + 7) / 8;
+    const int64_t total = (int64_t)M * nch;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = idx / nch;
+        const int j = (int)(idx - i * nch) * 8;
+        _Float16 *row = C + i * ldc + j;
+        if (VEC && j + 8 <= N) {
+            h8 c = *reinterpret_cast<const h8 *>(row);
+            h8 b = *reinterpret_cast<const h8 *>(bias + j);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) c[e] = (_Float16)((float)c[e] + (float)b[e]);
+            *reinterpret_cast<h8 *>(row) = c;
+        } else {
+            for (int e = 0; e < 8 && j + e < N; ++e)
+                row[e] = (_Float16)((float)row[e] + (float)bias[j + e]);
+        }
+    }
+}
+
+template <bool VEC>
+__global__ void __launch_bounds__(256) relu_kernel(_Float16 *C, int64_t ldc, int M, int N)
+{
+    const int64_t nch = (N + 7) / 8;
+    const int64_t total = (int64_t)M * nch;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = idx / nch;
+        const int j = (int)(idx - i * nch) * 8;
+        _Float16 *row = C + i * ldc + j;
+        if (VEC && j + 8 <= N) {
+            h8 c = *reinterpret_cast<const h8 *>(row);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) c[e] = c[e] > (_Float16)0.0f ? c[e] : (_Float16)0.0f;
+            *reinterpret_cast<h8 *>(row) = c;
+        } else {
+            for (int e = 0; e < 8 && j + e < N; ++e)
+                row[e] = row[e] > (_Float16)0.0f ? row[e] : (_Float16)0.0f;
+        }
+    }
+}
+
+unsigned pointwise_grid(int64_t M, int64_t N)
+{
+    int64_t chunks = M * ((N + 7) / 8);
+    int64_t blocks = ceil_div(chunks, 256);
+    return (unsigned)(blocks < 65536 ? (blocks > 0 ? blocks : 1) : 65536);
+}
+
+gba_status validate_pointwise(int64_t M, int64_t N, const void *C, int64_t ldc, const void *bias,
+                              bool need_bias)
+{
+    if (M < 0 || N < 0 || ldc < 0) return GBA_EINVAL;
+    if (M > INT_MAX || N > INT_MAX) return GBA_EUNSUPPORTED;
+    if (M == 0 || N == 0) return GBA_OK;
+    if (C == nullptr || ldc < N || (need_bias && bias == nullptr)) return GBA_EINVAL;
+    if (!aligned(C, 2) || !aligned(bias, 2)) return GBA_EUNSUPPORTED;
+    return GBA_OK;
+}
+
+}  // namespace
+}  // namespace gba
+
+using namespace gba;
+
+extern "C" gba_status gemm_bias_act(gba_layout layoutA, gba_layout layoutB, int64_t M, int64_t N,
+                                    int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
+                                    const void *bias, void *C, int64_t ldc, gba_act act,
+                                    gba_acc accum, gba_stream_t stream)
+{
+    return run_gemm(layoutA, layoutB, M, N, K, A, lda, B, ldb, bias, C, ldc, act, accum, -1,
+                    reinterpret_cast<hipStream_t>(stream));
+}
+
+extern "C" gba_status gemm_bias_act_tile(gba_layout layoutA, gba_layout layoutB, int64_t M,
+                                         int64_t N, int64_t K, const void *A, int64_t lda,
+                                         const void *B, int64_t ldb, const void *bias, void *C,
+                                         int64_t ldc, gba_act act, gba_acc accum, int tile_id,
+                                         gba_stream_t stream)
+{
+    return run_gemm(layoutA, layoutB, M, N, K, A, lda, B, ldb, bias, C, ldc, act, accum, tile_id,
+                    reinterpret_cast<hipStream_t>(stream));
+}
+
+extern "C" int gba_num_tiles(void) { return NUM_TILES; }
+
+extern "C" gba_status gba_tile_info(int tile_id, int *bm, int *bn, int *bk, int *waves, int *split_k)
+{
+    if (tile_id < 0 || tile_id >= NUM_TILES) return GBA_EINVAL;
+    const TileCfg &c = TILES[tile_id];
+    if (bm) *bm = c.bm;
+    if (bn) *bn = c.bn;
+    if (bk) *bk = 64;
+    if (waves) *waves = c.wm * c.wn;
+    if (split_k) *split_k = 1;
+    return GBA_OK;
+}
+
+extern "C" int gba_select_tile(gba_layout layoutA, gba_layout layoutB, int64_t M, int64_t N, int64_t K,
+                               gba_acc accum)
+{
+    if (!is_layout(layoutA) || !is_layout(layoutB)) return -1;
+    if (accum != GBA_ACC_F32 && accum != GBA_ACC_F16) return -1;
+    if (M < 0 || N < 0 || K < 0 || M > INT_MAX || N > INT_MAX || K > INT_MAX) return -1;
+    return select_tile(M, N, K);
+}
+
+extern "C" gba_status gba_bias_add_f16(int64_t M, int64_t N, void *C, int64_t ldc, const void *bias,
+                                       gba_stream_t stream)
+{
+    gba_status st = validate_pointwise(M, N, C, ldc, bias, true);
+    if (st != GBA_OK || M == 0 || N == 0) return st;
+    const bool vec = aligned(C, 16) && aligned(bias, 16) && ldc % 8 == 0;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    dim3 grid(pointwise_grid(M, N)), block(256);
+    _Float16 *c = static_cast<_Float16 *>(C);
+    const _Float16 *b = static_cast<const _Float16 *>(bias);
+    if (vec)
+        hipLaunchKernelGGL(bias_add_kernel<true>, grid, block, 0, s, c, ldc, b, (int)M, (int)N);
+    else
+        hipLaunchKernelGGL(bias_add_kernel<false>, grid, block, 0, s, c, ldc, b, (int)M, (int)N);
+    return hipGetLastError() == hipSuccess ? GBA_OK : GBA_EHIP;
+}
+
+extern "C" gba_status gba_relu_f16(int64_t M, int64_t N, void *C, int64_t ldc, gba_stream_t stream)
+{
+    gba_status st = validate_pointwise(M, N, C, ldc, nullptr, false);
+    if (st != GBA_OK || M == 0 || N == 0) return st;
+    const bool vec = aligned(C, 16) && ldc % 8 == 0;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    dim3 grid(pointwise_grid(M, N)), block(256);
+    _Float16 *c = static_cast<_Float16 *>(C);
+    if (vec)
+        hipLaunchKernelGGL(relu_kernel<true>, grid, block, 0, s, c, ldc, (int)M, (int)N);
+    else
+        hipLaunchKernelGGL(relu_kernel<false>, grid, block, 0, s, c, ldc, (int)M, (int)N);
+    return hipGetLastError() == hipSuccess ? GBA_OK : GBA_EHIP;
+}
+
+extern "C" const char *gba_status_string(gba_status status)
+{
+    switch (status) {
+    case GBA_OK: return "GBA_OK";
+    case GBA_EINVAL: return "GBA_EINVAL: invalid argument";
+    case GBA_EUNSUPPORTED: return "GBA_EUNSUPPORTED: unsupported argument";
+    case GBA_EHIP: return "GBA_EHIP: HIP launch error";
+    }
+    return "unknown gba_status";
+}
+
+extern "C" const char *gba_version(void) { return "gba 0.1.0 gfx950"; }

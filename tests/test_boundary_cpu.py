@@ -1,0 +1,135 @@
+"""The C ABI on the CPU: the library loads, exports every declared symbol,
+and rejects bad arguments before touching the GPU.  No compute call is made
+here (there is no GPU in this environment)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2006_12645_amd import gba
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gba.h")
+
+FAKE = 0x10000  # a 16-byte aligned non-null address; never dereferenced here
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_expected_api():
+    fns = declared_functions()
+    assert "gemm_bias_act" in fns and "gba_bias_add_f16" in fns and "gba_relu_f16" in fns
+    assert set(fns) == set(gba.SIGNATURES), (fns, sorted(gba.SIGNATURES))
+
+
+def test_library_exports_every_declared_symbol():
+    L = ctypes.CDLL(gba.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def gemm(M=64, N=64, K=64, la=0, lb=1, A=FAKE, lda=None, B=FAKE, ldb=None, bias=None, C=FAKE,
+         ldc=None, act=1, acc=0, tile=None):
+    lda = (K if la == 0 else M) if lda is None else lda
+    ldb = (N if lb == 0 else K) if ldb is None else ldb
+    ldc = N if ldc is None else ldc
+    args = [la, lb, M, N, K, A, lda, B, ldb, bias, C, ldc, act, acc]
+    if tile is None:
+        return gba.lib().gemm_bias_act(*args, None)
+    return gba.lib().gemm_bias_act_tile(*args, tile, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(M=-1), gba.GBA_EINVAL),
+    (dict(N=-5), gba.GBA_EINVAL),
+    (dict(K=-1), gba.GBA_EINVAL),
+    (dict(la=2), gba.GBA_EINVAL),
+    (dict(lb=-1), gba.GBA_EINVAL),
+    (dict(act=7), gba.GBA_EINVAL),
+    (dict(acc=3), gba.GBA_EINVAL),
+    (dict(ldc=63), gba.GBA_EINVAL),
+    (dict(lda=63), gba.GBA_EINVAL),
+    (dict(la=1, lda=63), gba.GBA_EINVAL),
+    (dict(ldb=63), gba.GBA_EINVAL),
+    (dict(lb=0, ldb=63), gba.GBA_EINVAL),
+    (dict(A=None), gba.GBA_EINVAL),
+    (dict(B=None), gba.GBA_EINVAL),
+    (dict(C=None), gba.GBA_EINVAL),
+    (dict(tile=8), gba.GBA_EINVAL),
+    (dict(tile=1000), gba.GBA_EINVAL),
+    (dict(A=FAKE + 1), gba.GBA_EUNSUPPORTED),
+    (dict(C=FAKE + 1), gba.GBA_EUNSUPPORTED),
+    (dict(bias=FAKE + 1), gba.GBA_EUNSUPPORTED),
+    (dict(M=2**31), gba.GBA_EUNSUPPORTED),
+    (dict(K=2**31, lda=2**31), gba.GBA_EUNSUPPORTED),
+    # empty output: accepted, nothing launched (NULL operands are fine)
+    (dict(M=0, A=None, B=None, C=None), gba.GBA_OK),
+    (dict(N=0, A=None, B=None, C=None), gba.GBA_OK),
+    (dict(M=0, tile=3), gba.GBA_OK),
+])
+def test_gemm_validation(kw, status):
+    assert gemm(**kw) == status
+
+
+def test_pointwise_validation():
+    L = gba.lib()
+    assert L.gba_bias_add_f16(-1, 4, FAKE, 4, FAKE, None) == gba.GBA_EINVAL
+    assert L.gba_bias_add_f16(4, 4, None, 4, FAKE, None) == gba.GBA_EINVAL
+    assert L.gba_bias_add_f16(4, 4, FAKE, 4, None, None) == gba.GBA_EINVAL
+    assert L.gba_bias_add_f16(4, 8, FAKE, 4, FAKE, None) == gba.GBA_EINVAL
+    assert L.gba_bias_add_f16(4, 4, FAKE + 1, 4, FAKE, None) == gba.GBA_EUNSUPPORTED
+    assert L.gba_bias_add_f16(0, 4, None, 4, None, None) == gba.GBA_OK
+    assert L.gba_relu_f16(4, -4, FAKE, 4, None) == gba.GBA_EINVAL
+    assert L.gba_relu_f16(4, 4, None, 4, None) == gba.GBA_EINVAL
+    assert L.gba_relu_f16(2**31, 4, FAKE, 4, None) == gba.GBA_EUNSUPPORTED
+    assert L.gba_relu_f16(4, 0, None, 0, None) == gba.GBA_OK
+
+
+def test_tile_table():
+    n = gba.num_tiles()
+    assert n >= 1
+    for t in range(n):
+        info = gba.tile_info(t)
+        assert info["bm"] % 16 == 0 and info["bn"] % 32 == 0 and info["bk"] % 32 == 0
+        assert 1 <= info["waves"] <= 16 and info["split_k"] >= 1
+        # two LDS stages of (bm + bn) x bk fp16 fit in a gfx950 CU's 160 KB
+        assert 2 * (info["bm"] + info["bn"]) * info["bk"] * 2 <= 160 * 1024
+    with pytest.raises(gba.GbaError):
+        gba.tile_info(n)
+
+
+@pytest.mark.parametrize("shape", [(128, 128, 128), (1024, 1024, 1024), (4096, 4096, 4096),
+                                   (8192, 4096, 1024), (8192, 1024, 4096), (32, 4096, 1024),
+                                   (128, 4096, 1024), (256, 4096, 1024), (1000, 1000, 1000),
+                                   (1, 1, 1), (0, 5, 5)])
+def test_select_tile(shape):
+    t = gba.select_tile(*shape)
+    assert 0 <= t < gba.num_tiles()
+
+
+def test_select_tile_rejects_bad_input():
+    assert gba.lib().gba_select_tile(0, 1, -1, 4, 4, 0) == -1
+    assert gba.lib().gba_select_tile(5, 1, 1, 4, 4, 0) == -1
+    assert gba.lib().gba_select_tile(0, 1, 1, 4, 4, 9) == -1
+
+
+def test_status_strings_and_version():
+    for s in range(4):
+        assert gba.lib().gba_status_string(s)
+    assert b"unknown" in gba.lib().gba_status_string(99)
+    assert "gfx950" in gba.version()
+
+
+def test_layout_inference_on_cpu_tensors():
+    import torch
+    a = torch.zeros(6, 10, dtype=torch.float16)
+    assert gba.operand_layout(a, 6, 10) == (gba.GBA_ROW_MAJOR, 10)
+    assert gba.operand_layout(a.t(), 10, 6) == (gba.GBA_COL_MAJOR, 10)
+    assert gba.operand_layout(a[:, :7], 6, 7) == (gba.GBA_ROW_MAJOR, 10)
+    with pytest.raises(ValueError):
+        gba.operand_layout(a[::2, ::2], 3, 5)

@@ -1,0 +1,292 @@
+"""HIP path vs the CPU oracle, element by element, through the C ABI.
+
+Each case prints its name, shape and seed before touching the GPU so a
+failing run names the case.  Inputs come from the seeded generators in
+paper_2006_12645_amd.datagen; expected values from the oracle only.
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2006_12645_amd import datagen as D
+from paper_2006_12645_amd import gba
+
+import gpu_util as U
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+LAYOUTS = ["RR", "RC", "CR", "CC"]
+
+
+def announce(*what):
+    print("CASE", *what, flush=True)
+
+
+def run_gpu(A, B, bias, layout, act="relu", accum="f32", tile=None, pad=0, out=None, stream=None):
+    la, lb = D.LAYOUT_NAMES[layout]
+    dA = U.device_operand(A, la, pad)
+    dB = U.device_operand(B, lb, pad)
+    dbias = None if bias is None else torch.from_numpy(bias).cuda()
+    o = gba.gemm_bias_act(dA, dB, dbias, act=act, accum=accum, tile=tile, out=out, stream=stream)
+    torch.cuda.synchronize()
+    return o
+
+
+def sample_rows(M, seed, count=24):
+    rng = np.random.default_rng(seed)
+    rows = {0, M - 1, M // 2}
+    for edge in (128, 256):
+        rows.update(r for r in (edge - 1, edge, M - edge) if 0 <= r < M)
+    rows.update(int(r) for r in rng.integers(0, M, size=count))
+    return sorted(rows)
+
+
+@pytest.fixture(autouse=True, scope="module")
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    gba.lib()
+    yield
+
+
+# ----------------------------------------------------------------------------
+# The five workload families
+
+def test_cube128_rc():
+    w = D.WORKLOADS["cube128_RC"]
+    announce(w.name)
+    A, B, bias = D.logical_inputs(w)
+    got = run_gpu(A, B, bias, "RC").cpu().numpy()
+    U.assert_close(got, U.oracle_for(A, B, bias), what=w.name)
+
+
+@pytest.fixture(scope="module")
+def cube1024():
+    w = D.WORKLOADS["cube1024_all_layouts"]
+    A, B, bias = D.logical_inputs(w)
+    return A, B, bias, U.oracle_for(A, B, bias)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_cube1024_layouts(cube1024, layout):
+    A, B, bias, ref = cube1024
+    announce("cube1024", layout)
+    U.assert_close(run_gpu(A, B, bias, layout).cpu().numpy(), ref, what=f"1024^3 {layout}")
+
+
+@pytest.fixture(scope="module")
+def cube4096():
+    w = D.WORKLOADS["cube4096_RC"]
+    A, B, bias = D.logical_inputs(w)
+    rows = sample_rows(w.M, 4096)
+    return A, B, bias, rows
+
+
+def test_cube4096_fused_sampled(cube4096):
+    A, B, bias, rows = cube4096
+    announce("cube4096 fused RC rows", len(rows))
+    got = run_gpu(A, B, bias, "RC").cpu().numpy()[rows]
+    U.assert_close(got, U.oracle_for(A, B, bias, rows=rows), what="4096^3 fused")
+
+
+def test_cube4096_plain_sampled(cube4096):
+    A, B, _, rows = cube4096
+    announce("cube4096 plain RC")
+    got = run_gpu(A, B, None, "RC", act="none").cpu().numpy()[rows]
+    U.assert_close(got, U.oracle_for(A, B, None, act=O.ACT_NONE, rows=rows), what="4096^3 plain")
+
+
+def test_cube4096_unfused_sampled(cube4096):
+    A, B, bias, rows = cube4096
+    announce("cube4096 unfused RC")
+    dA = U.device_operand(A, D.ROW)
+    dB = U.device_operand(B, D.COL)
+    out = gba.unfused_gemm_bias_relu(dA, dB, torch.from_numpy(bias).cuda())
+    torch.cuda.synchronize()
+    U.assert_close(out.cpu().numpy()[rows], U.oracle_for(A, B, bias, rows=rows), what="unfused")
+
+
+@pytest.mark.parametrize("name", ["mlp_up_8192x4096x1024", "mlp_down_8192x1024x4096"])
+def test_mlp_sampled(name):
+    w = D.WORKLOADS[name]
+    announce(name)
+    A, B, bias = D.logical_inputs(w)
+    rows = sample_rows(w.M, w.seed_base)
+    got = run_gpu(A, B, bias, "RC").cpu().numpy()[rows]
+    U.assert_close(got, U.oracle_for(A, B, bias, rows=rows), what=name)
+
+
+@pytest.mark.parametrize("name", ["infer_m32_n4096_k1024", "infer_m128_n4096_k1024",
+                                  "infer_m256_n4096_k1024"])
+@pytest.mark.parametrize("accum", ["f32", "f16"])
+def test_inference_shapes(name, accum):
+    w = D.WORKLOADS[name]
+    announce(name, accum)
+    A, B, bias = D.logical_inputs(w)
+    got = run_gpu(A, B, bias, "RC", accum=accum).cpu().numpy()
+    U.assert_close(got, U.oracle_for(A, B, bias), accum=accum, what=f"{name} {accum}")
+
+
+@pytest.fixture(scope="module")
+def ragged():
+    w = D.WORKLOADS["ragged1000"]
+    A, B, bias = D.logical_inputs(w)
+    return A, B, bias, U.oracle_for(A, B, bias)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("accum", ["f32", "f16"])
+def test_ragged1000(ragged, layout, accum):
+    A, B, bias, ref = ragged
+    announce("ragged1000", layout, accum)
+    got = run_gpu(A, B, bias, layout, accum=accum).cpu().numpy()
+    U.assert_close(got, ref, accum=accum, what=f"1000^3 {layout} {accum}")
+
+
+# ----------------------------------------------------------------------------
+# Exactness, tiles, edges
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("accum", ["f32", "f16"])
+def test_integer_data_bit_exact(layout, accum):
+    """{-1,0,1} operands and integer bias: every partial sum is an integer
+    below 2048, exact in fp16 and fp32, so the result must equal the oracle
+    exactly whatever the summation order or accumulator precision."""
+    M, N, K = 300, 260, 1000
+    announce("integer exact", layout, accum, M, N, K)
+    A, B, bias = D.random_problem(77, M, N, K, dist="int")
+    got = run_gpu(A, B, bias, layout, accum=accum).cpu().numpy().astype(np.float64)
+    assert np.array_equal(got, U.oracle_for(A, B, bias))
+
+
+@pytest.mark.parametrize("tile", range(8))
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_every_tile_config(tile, layout):
+    M, N, K = 300, 330, 200
+    announce("tile", tile, layout)
+    A, B, bias = D.random_problem(1000 + tile, M, N, K)
+    got = run_gpu(A, B, bias, layout, tile=tile).cpu().numpy()
+    U.assert_close(got, U.oracle_for(A, B, bias), what=f"tile {tile} {layout}")
+
+
+@pytest.mark.parametrize("tile", range(8))
+def test_every_tile_config_f16acc(tile):
+    M, N, K = 130, 250, 515
+    announce("tile f16acc", tile)
+    A, B, bias = D.random_problem(1100 + tile, M, N, K)
+    got = run_gpu(A, B, bias, "RC", accum="f16", tile=tile).cpu().numpy()
+    U.assert_close(got, U.oracle_for(A, B, bias), accum="f16", what=f"tile {tile} f16")
+
+
+RAGGED = [1, 7, 31, 33, 127, 129]
+
+
+@pytest.mark.parametrize("M", RAGGED)
+@pytest.mark.parametrize("N", [1, 33, 129])
+@pytest.mark.parametrize("K", [7, 33, 129])
+def test_ragged_sizes_guarded(M, N, K):
+    """Odd sizes in every dimension (scalar path when a leading dimension is
+    not a multiple of 8), with a sentinel-filled guard band around C that
+    must come back untouched."""
+    announce("ragged", M, N, K)
+    A, B, bias = D.random_problem(M * 10000 + N * 100 + K, M, N, K)
+    pad = (-K) % 8 if K % 8 else 0
+    G = 8
+    big = torch.full((M + 2 * G, N + 2 * G), 12345.0, dtype=torch.float16, device="cuda")
+    out = big[G:G + M, G:G + N]
+    for layout in LAYOUTS:
+        big.fill_(12345.0)
+        run_gpu(A, B, bias, layout, out=out, pad=pad)
+        host = big.cpu().numpy()
+        inner = host[G:G + M, G:G + N]
+        U.assert_close(inner, U.oracle_for(A, B, bias), what=f"{M}x{N}x{K} {layout}")
+        guard = host.copy()
+        guard[G:G + M, G:G + N] = 12345.0
+        assert (guard == np.float16(12345.0)).all(), "write outside C"
+
+
+def test_unaligned_operands_take_scalar_path():
+    M, N, K = 200, 150, 300
+    announce("unaligned")
+    A, B, bias = D.random_problem(55, M, N, K)
+    ref = U.oracle_for(A, B, bias)
+    for layout in LAYOUTS:
+        la, lb = D.LAYOUT_NAMES[layout]
+        # operands shifted by one fp16 element inside a larger buffer
+        sa = D.store(A, la, (K if la == D.ROW else M) + 3)
+        sb = D.store(B, lb, (N if lb == D.ROW else K) + 3)
+        # storage that starts one fp16 element past a 16-byte boundary
+        ta = torch.empty(1 + sa.size, dtype=torch.float16, device="cuda")
+        tb = torch.empty(1 + sb.size, dtype=torch.float16, device="cuda")
+        ta[1:] = torch.from_numpy(sa.ravel()).cuda()
+        tb[1:] = torch.from_numpy(sb.ravel()).cuda()
+        ta, tb = ta[1:], tb[1:]
+        lda, ldb = sa.shape[1], sb.shape[1]
+        dA = (ta.as_strided((M, K), (lda, 1)) if la == D.ROW else ta.as_strided((M, K), (1, lda)))
+        dB = (tb.as_strided((K, N), (ldb, 1)) if lb == D.ROW else tb.as_strided((K, N), (1, ldb)))
+        got = gba.gemm_bias_act(dA, dB, torch.from_numpy(bias).cuda(), act="relu")
+        torch.cuda.synchronize()
+        U.assert_close(got.cpu().numpy(), ref, what=f"unaligned {layout}")
+
+
+def test_k_zero_gives_activation_of_bias():
+    M, N = 70, 90
+    announce("K=0")
+    bias = D.uniform_f16(5, (N,))
+    A = torch.zeros((M, 0), dtype=torch.float16, device="cuda")
+    B = torch.zeros((0, N), dtype=torch.float16, device="cuda")
+    for act in ("relu", "none"):
+        got = gba.gemm_bias_act(A, B, torch.from_numpy(bias).cuda(), act=act)
+        torch.cuda.synchronize()
+        want = np.maximum(bias.astype(np.float64), 0) if act == "relu" else bias.astype(np.float64)
+        assert np.array_equal(got.cpu().numpy().astype(np.float64), np.broadcast_to(want, (M, N)))
+
+
+def test_no_bias_no_activation_matches_oracle():
+    M, N, K = 257, 511, 384
+    announce("plain")
+    A, B, _ = D.random_problem(66, M, N, K)
+    for layout in LAYOUTS:
+        got = run_gpu(A, B, None, layout, act="none").cpu().numpy()
+        U.assert_close(got, U.oracle_for(A, B, None, act=O.ACT_NONE), what=f"plain {layout}")
+
+
+def test_relu_output_properties():
+    M, N, K = 512, 512, 512
+    announce("relu props")
+    A, B, bias = D.random_problem(67, M, N, K)
+    got = run_gpu(A, B, bias, "RC").cpu().numpy().astype(np.float64)
+    pre = U.oracle_for(A, B, bias, act=O.ACT_NONE)
+    assert (got >= 0).all()
+    assert (got[pre < -0.02] == 0).all()
+    assert ((got > 0) == (pre > 0))[np.abs(pre) > 0.02].all()
+
+
+def test_deterministic_and_stream():
+    M, N, K = 1024, 768, 512
+    announce("determinism")
+    A, B, bias = D.random_problem(68, M, N, K)
+    a = run_gpu(A, B, bias, "RC")
+    b = run_gpu(A, B, bias, "RC")
+    assert torch.equal(a, b)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        c = run_gpu(A, B, bias, "RC", stream=s)
+    s.synchronize()
+    assert torch.equal(a, c)
+
+
+def test_unfused_pieces():
+    M, N = 333, 1031
+    announce("pointwise")
+    C0 = D.uniform_f16(90, (M, N), -4, 4)
+    bias = D.uniform_f16(91, (N,))
+    C = torch.from_numpy(C0).cuda()
+    gba.bias_add_(C, torch.from_numpy(bias).cuda())
+    torch.cuda.synchronize()
+    want = (C0.astype(np.float32) + bias.astype(np.float32)).astype(np.float16)
+    assert np.array_equal(C.cpu().numpy(), want)
+    gba.relu_(C)
+    torch.cuda.synchronize()
+    assert np.array_equal(C.cpu().numpy(), np.maximum(want, np.float16(0)))
