@@ -44,11 +44,29 @@ int select_tile(int64_t M, int64_t N, int64_t K)
     (void)K;
     const int64_t CUS = 256;
     if (ceil_div(M, 256) * ceil_div(N, 256) >= CUS) return 0;
-    if (ceil_div(M, 256) * ceil_div(N, 128) >= CUS) return 3;
-    if (ceil_div(M, 128) * ceil_div(N, 128) >= CUS) return 2;
-    if (ceil_div(M, 64) * ceil_div(N, 128) >= CUS) return 7;
-    if (M <= 32) return 6;
-    return 5;
+    if (ceil_div(M, 256) * ceil_div(N, 128) >= CUS) return 2;
+    if (ceil_div(M, 128) * ceil_div(N, 256) >= CUS) return 3;
+    if (ceil_div(M, 128) * ceil_div(N, 128) >= CUS) return 4;
+    if (ceil_div(M, 128) * ceil_div(N, 64) >= CUS) return 5;
+    if (ceil_div(M, 64) * ceil_div(N, 64) >= CUS) return 6;
+    if (M <= 32) return N >= 4096 ? 8 : 9;
+    return 6;
+}
+
+// Largest leading dimension the fast path addresses with 32-bit offsets.
+constexpr int64_t FAST_MAX_LD = int64_t(1) << 21;
+
+// The fast path needs every 16-byte chunk of every operand wholly inside or
+// wholly outside the matrix.
+bool fast_path_ok(int la, int lb, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
+                  const void *B, int64_t ldb, const void *bias, const void *C, int64_t ldc)
+{
+    if (!aligned(A, 16) || !aligned(B, 16) || !aligned(C, 16) || !aligned(bias, 16)) return false;
+    if (lda % 8 || ldb % 8 || ldc % 8 || lda >= FAST_MAX_LD || ldb >= FAST_MAX_LD) return false;
+    if (N % 8) return false;
+    if ((la == GBA_ROW_MAJOR ? K : M) % 8) return false;
+    if ((lb == GBA_COL_MAJOR ? K : N) % 8) return false;
+    return true;
 }
 
 const LayoutTable &table_for(int la, int lb)
@@ -65,10 +83,9 @@ gba_status run_gemm(int la, int lb, int64_t M, int64_t N, int64_t K, const void 
     gba_status st = validate_gemm(la, lb, M, N, K, A, lda, B, ldb, bias, C, ldc, act, accum);
     if (st != GBA_OK || M == 0 || N == 0) return st;
 
-    const bool vec = aligned(A, 16) && aligned(B, 16) && aligned(C, 16) && aligned(bias, 16) &&
-                     lda % 8 == 0 && ldb % 8 == 0 && ldc % 8 == 0;
-    const int tile = !vec ? GENERIC_TILE : (tile_id >= 0 ? tile_id : select_tile(M, N, K));
-    const TileCfg &cfg = TILES[tile];
+    const bool fast = fast_path_ok(la, lb, M, N, K, A, lda, B, ldb, bias, C, ldc);
+    const int tile = fast ? (tile_id >= 0 ? tile_id : select_tile(M, N, K)) : -1;
+    const TileCfg cfg = fast ? TILES[tile] : GENERIC_TILE;
 
     GemmArgs a;
     a.A = static_cast<const _Float16 *>(A);
@@ -88,7 +105,7 @@ gba_status run_gemm(int la, int lb, int64_t M, int64_t N, int64_t K, const void 
 
     const LayoutTable &tab = table_for(la, lb);
     const int acc16 = accum == GBA_ACC_F16;
-    LaunchFn fn = vec ? tab.vec[tile][acc16] : tab.scalar[acc16];
+    LaunchFn fn = fast ? tab.fast[tile][acc16] : tab.generic[acc16];
     return fn(a, stream) == hipSuccess ? GBA_OK : GBA_EHIP;
 }
 

@@ -5,22 +5,18 @@
 
 namespace gba {
 
-#define GBA_VEC_ENTRY(id, BM, BN, WM, WN) \
-    {&launch_gemm<BM, BN, WM, WN, COL, COL, false, true>, &launch_gemm<BM, BN, WM, WN, COL, COL, true, true>},
+#define GBA_FAST_ENTRY(id, BM, BN, WM, WN) \
+    {&launch_fast<BM, BN, WM, WN, COL, COL, false>, &launch_fast<BM, BN, WM, WN, COL, COL, true>},
 
 const LayoutTable &table_CC()
 {
     static const LayoutTable t = {
-        {GBA_TILE_LIST(GBA_VEC_ENTRY)},
-        {&launch_gemm<64, 64, 2, 2, COL, COL, false, false>, &launch_gemm<64, 64, 2, 2, COL, COL, true, false>},
+        {GBA_TILE_LIST(GBA_FAST_ENTRY)},
+        {&launch_generic<COL, COL, false>, &launch_generic<COL, COL, true>},
     };
     return t;
 }
 
-#undef GBA_VEC_ENTRY
-
-static_assert(TILES[GENERIC_TILE].bm == 64 && TILES[GENERIC_TILE].bn == 64 &&
-                  TILES[GENERIC_TILE].wm == 2 && TILES[GENERIC_TILE].wn == 2,
-              "scalar entries are instantiated for the generic tile");
+#undef GBA_FAST_ENTRY
 
 }  // namespace gba

@@ -5,22 +5,18 @@
 
 namespace gba {
 
-#define GBA_VEC_ENTRY(id, BM, BN, WM, WN) \
-    {&launch_gemm<BM, BN, WM, WN, ROW, ROW, false, true>, &launch_gemm<BM, BN, WM, WN, ROW, ROW, true, true>},
+#define GBA_FAST_ENTRY(id, BM, BN, WM, WN) \
+    {&launch_fast<BM, BN, WM, WN, ROW, ROW, false>, &launch_fast<BM, BN, WM, WN, ROW, ROW, true>},
 
 const LayoutTable &table_RR()
 {
     static const LayoutTable t = {
-        {GBA_TILE_LIST(GBA_VEC_ENTRY)},
-        {&launch_gemm<64, 64, 2, 2, ROW, ROW, false, false>, &launch_gemm<64, 64, 2, 2, ROW, ROW, true, false>},
+        {GBA_TILE_LIST(GBA_FAST_ENTRY)},
+        {&launch_generic<ROW, ROW, false>, &launch_generic<ROW, ROW, true>},
     };
     return t;
 }
 
-#undef GBA_VEC_ENTRY
-
-static_assert(TILES[GENERIC_TILE].bm == 64 && TILES[GENERIC_TILE].bn == 64 &&
-                  TILES[GENERIC_TILE].wm == 2 && TILES[GENERIC_TILE].wn == 2,
-              "scalar entries are instantiated for the generic tile");
+#undef GBA_FAST_ENTRY
 
 }  // namespace gba

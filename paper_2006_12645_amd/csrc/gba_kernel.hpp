@@ -1,176 +1,168 @@
-// gba_kernel.hpp -- the fused fp16 GEMM + bias + activation kernel for gfx950.
+// gba_kernel.hpp -- the fast path of the fused fp16 GEMM + bias + activation
+// for gfx950, used when every operand is 16-byte aligned, the leading
+// dimensions are multiples of 8 and the contiguous extent of each operand is
+// a multiple of 8 (so every 16-byte chunk is either wholly inside the matrix
+// or wholly outside it).
 //
-// One workgroup computes one BM x BN tile of C (block tile, Tiling for Blocks
-// and Warps subsection); its waves each own a WTM x WTN sub-tile (warp tile).
-// The reduction dimension is walked in steps of BK = 64 (strip-mining of the
-// sequential dimension), staged global -> registers -> LDS (Global to Shared
-// Memory subsection) with the next step's global loads in flight while the
-// current step is multiplied (Prefetching and Hiding Latency subsection).
-// Each 32-deep slice of a step is one wave-wide v_mfma_f32_16x16x32_f16 per
-// 16x16 output block: the CDNA4 matrix instruction plays the role of the
-// paper's composed macro-MMA.  After the last step the bias add, ReLU and
-// fp16 conversion run on the accumulator registers and each lane stores 8
-// contiguous fp16 values (Pointwise Operations in Epilogue subsection): the
-// matmul result never reaches global memory.
+// Structure (Matmul Compute Decomposition and Data Movement sections):
+//   * A workgroup owns a BM x BN block tile of C, its WM x WN waves a
+//     (BM/WM) x (BN/WN) warp tile each; the reduction runs in steps of
+//     BK = 64 (strip-mining of the sequential dimension).
+//   * Each step's A and B tiles go global -> registers -> LDS (the split copy
+//     of the Global to Shared Memory subsection) through 16-byte buffer
+//     loads; the next step's loads are in flight while the current step is
+//     multiplied (Prefetching and Hiding Latency subsection) and LDS is
+//     double-buffered, so one barrier per step suffices.
+//   * The wave-level contraction is v_mfma_f32_32x32x16_f16: fp16 inputs,
+//     fp32 accumulation, a 32x32 output block per instruction -- the CDNA4
+//     counterpart of the paper's 32x32x8 macro-MMA.  A 16-deep slice of k is
+//     one instruction per 32x32 block (the outer-product order of the
+//     strip-mined warp MMA).
+//   * After the last step the accumulators get the bias add, ReLU and fp16
+//     conversion in registers, and each lane stores 16 contiguous outputs as
+//     two 16-byte writes (Pointwise Operations in Epilogue subsection): the
+//     matmul result never reaches global memory.
 //
-// Operand roles.  The MFMA "A" slot (rows indexed by lane % 16) is fed with
-// columns of B, the "B" slot (columns indexed by lane % 16) with rows of A,
-// so the instruction produces a block of C transposed: lane l holds four
-// consecutive output COLUMNS of one output row.  A permutation of the B
-// columns inside each 32-column pair of blocks (jperm below) makes those two
-// groups of four adjacent, so every lane owns 8 contiguous fp16 outputs and
-// stores them with one 16-byte write -- the role the paper gives to its
-// reordering through shared memory, done here without any shared memory.
+// Operand roles.  The MFMA "A" slot (rows = lane % 32) is fed with columns
+// of B and the "B" slot (columns = lane % 32) with rows of A, so each
+// instruction yields a block of C transposed: lane l's 16 accumulators are 16
+// output columns of output row l % 32.  Inside each 32-column block the B
+// columns are presented to the MFMA in the order jp32 so that those 16
+// columns are consecutive -- the wide-store reordering that the paper does
+// through shared memory, obtained here for free.
 //
-// LDS layout.  Both operand tiles are stored reduction-contiguous: a row of
-// 64 fp16 (128 bytes = 8 chunks of 16 bytes) per output row or column, and
-// chunk c of row r lives at chunk position c ^ swz(r).  swz is a bijection on
-// chunks per row chosen so that (a) 8 lanes writing one row, (b) lanes
-// writing the same chunk of 8-row-strided rows (transposed staging), (c)
-// 16 consecutive rows read at one chunk, and (d) the jperm-ordered reads of
-// the B tile all touch distinct banks (Swizzled Shared Memory subsection).
+// LDS.  Both tiles are stored reduction-contiguous, one 128-byte row (64
+// fp16 = 8 chunks of 16 bytes) per output row / column; chunk c of row r is
+// kept at chunk position c ^ swz32(r) (Swizzled Shared Memory subsection).
+// swz32 depends on r mod 32 only, so fragment addresses differ between
+// blocks by constants, and it makes the fragment reads and the row-wise
+// staging writes free of bank conflicts.
 //
-// Layouts.  When an operand is stored reduction-contiguous in global memory
-// (row-major A, column-major B) a lane copies 16-byte chunks straight through.
-// Otherwise (column-major A, row-major B) a lane loads an 8 x 8 block as 8
-// row chunks, transposes it in registers and writes 8 reduction-contiguous
-// chunks: the four per-layout copy helpers of the Global to Shared Memory
-// subsection.
+// Layouts.  A reduction-contiguous operand (row-major A, column-major B) is
+// copied chunk by chunk.  For the other two cases a lane loads an 8 x 8
+// block of fp16 as 8 chunks along M (or N), transposes it in registers and
+// writes 8 reduction-contiguous chunks: the per-layout copy helpers.
 //
-// Edges.  Rows/columns beyond M or N and reduction indices beyond K are
-// loaded as zeros and out-of-range outputs are not stored, so any size is
-// handled in the kernel (the partial-tile case of the Tiling subsection).
+// Edges.  Out-of-range chunks are fetched through a buffer resource with an
+// offset beyond its size, which the hardware returns as zeros without a
+// branch; out-of-range outputs are not stored.
 #pragma once
 
-#include <hip/hip_runtime.h>
-#include <stdint.h>
+#include "gba_common.hpp"
 
 namespace gba {
 
-typedef _Float16 h8 __attribute__((ext_vector_type(8)));
-typedef float f4 __attribute__((ext_vector_type(4)));
+// Raw (unswizzled, stride 0) buffer resource with range checking.
+constexpr int RSRC_WORD3 = 0x00020000;
+// Offset of a chunk that must read as zero: beyond every resource's size.
+constexpr int OOB_OFFSET = (int)0x80000000u;
+constexpr int MAX_RECORDS = 0x7fffffff;
 
-enum { ROW = 0, COL = 1 };
-
-struct GemmArgs {
-    const _Float16 *A;
-    const _Float16 *B;
-    const _Float16 *bias;  // may be null
-    _Float16 *C;
-    int64_t lda, ldb, ldc;
-    int M, N, K;
-    int relu;
-    int tiles_m, tiles_n;
-};
-
-// Bijective chunk permutation per LDS row (see header comment).
-__device__ __forceinline__ int swz(int r)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const _Float16 *base, int64_t bytes)
 {
-    int b0 = ((r >> 2) ^ (r >> 3)) & 1;
-    int b1 = (r ^ (r >> 1) ^ (r >> 4)) & 1;
-    int b2 = ((r >> 1) ^ (r >> 3) ^ (r >> 5)) & 1;
+    int n = bytes > MAX_RECORDS ? MAX_RECORDS : (bytes < 0 ? 0 : (int)bytes);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<_Float16 *>(base), (short)0, n, RSRC_WORD3);
+}
+
+__device__ __forceinline__ h8 buffer_load16(__amdgpu_buffer_rsrc_t r, int voff)
+{
+    return __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
+}
+
+// Chunk permutation of LDS row r (periodic in 32 rows).
+__device__ __forceinline__ int swz32(int r)
+{
+    int b0 = ((r >> 2) ^ (r >> 4)) & 1;
+    int b1 = (r ^ (r >> 2) ^ (r >> 3)) & 1;
+    int b2 = (r >> 1) & 1;
     return b0 | (b1 << 1) | (b2 << 2);
 }
 
-// Position of MFMA row rho of block t inside a wave's run of B columns: two
-// neighbouring blocks share 32 columns so that a lane's 2 x 4 results are 8
-// consecutive columns.
-__device__ __forceinline__ int jperm(int t, int rho)
-{
-    return 32 * (t >> 1) + 8 * (rho >> 2) + 4 * (t & 1) + (rho & 3);
-}
+// Column (inside a 32-column block of B) presented as MFMA row rho.  The
+// MFMA returns row rho = 8*(r/4) + 4*(lane/32) + r%4 in accumulator r of a
+// lane, which this maps to column 16*(lane/32) + r.
+__device__ __forceinline__ int jp32(int rho) { return 16 * ((rho >> 2) & 1) + 4 * (rho >> 3) + (rho & 3); }
 
-__device__ __forceinline__ h8 zero_h8()
-{
-    h8 z;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) z[e] = (_Float16)0.0f;
-    return z;
-}
-
-// Eight consecutive fp16 from p[0..7], the ones at index >= lim read as 0.
-template <bool VEC>
-__device__ __forceinline__ h8 load8(const _Float16 *p, int lim)
-{
-    if (VEC && lim >= 8) return *reinterpret_cast<const h8 *>(p);
-    h8 v;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = e < lim ? p[e] : (_Float16)0.0f;
-    return v;
-}
-
-// Global -> register -> LDS copy of one operand tile of R rows (output rows
-// for A, output columns for B) by BK reduction indices.
-//   KCONT: the operand is reduction-contiguous in global memory.
-// X points at the operand, ld is its leading dimension, r0/k0 the tile origin,
-// rtot/ktot the extents.
-template <int R, int BK, int NT, bool KCONT, bool VEC>
-struct TileCopy {
-    static constexpr int CHUNKS = R * BK / 8;                 // 16-byte chunks per tile
-    static constexpr int KCH = BK / 8;                        // chunks per LDS row
-    static constexpr int PER = KCONT ? (CHUNKS + NT - 1) / NT // chunks per thread
-                                     : (CHUNKS / 8 + NT - 1) / NT;  // 8x8 blocks per thread
+// One operand tile of R rows (output rows of A, or output columns of B) by
+// 64 reduction indices: per-thread chunk offsets, staging registers, and the
+// register -> LDS write.
+//   KCONT: reduction-contiguous in global memory (row-major A, col-major B).
+template <int R, int NT, bool KCONT>
+struct FastStage {
+    static constexpr int CHUNKS = R * 8;
+    static constexpr int BLOCKS = R;  // 8 x 8 blocks when transposing
+    static constexpr int PER = KCONT ? CHUNKS / NT : (BLOCKS + NT - 1) / NT;
     static constexpr int NREG = KCONT ? PER : PER * 8;
+    static_assert(!KCONT || CHUNKS % NT == 0, "chunks must divide evenly among the threads");
+
+    int voff[NREG];      // byte offset of each chunk from the tile origin (or OOB_OFFSET)
+    int kchunk[KCONT ? PER : 1];  // reduction chunk index (KCONT tail masking)
+    int lds_off[KCONT ? PER : PER * 8];  // LDS byte offset of each written chunk
     h8 v[NREG];
 
-    __device__ __forceinline__ void load(const _Float16 *X, int64_t ld, int r0, int k0, int rtot,
-                                         int ktot, int tid)
+    __device__ __forceinline__ void init(int64_t ld, int r0, int rtot, int tid)
     {
         if constexpr (KCONT) {
 #pragma unroll
             for (int p = 0; p < PER; ++p) {
                 int idx = tid + p * NT;
-                int r = idx / KCH, c = idx % KCH;
-                int gr = r0 + r, gk = k0 + 8 * c;
-                h8 x = zero_h8();
-                if ((CHUNKS % NT == 0 || idx < CHUNKS) && gr < rtot && gk < ktot)
-                    x = load8<VEC>(X + (int64_t)gr * ld + gk, ktot - gk);
-                v[p] = x;
+                int r = idx >> 3, c = idx & 7;
+                voff[p] = r0 + r < rtot ? (int)(((int64_t)r * ld + 8 * c) * 2) : OOB_OFFSET;
+                kchunk[p] = c;
+                lds_off[p] = (r * 8 + (c ^ swz32(r))) * 16;
             }
         } else {
-            constexpr int RB = R / 8;
 #pragma unroll
             for (int p = 0; p < PER; ++p) {
                 int idx = tid + p * NT;
-                int rb = idx % RB, kb = idx / RB;
-                int gr = r0 + 8 * rb, gk0 = k0 + 8 * kb;
-                bool live = (CHUNKS / 8) % NT == 0 || idx < CHUNKS / 8;
+                int rb = idx % (R / 8), kb = idx / (R / 8);
+                bool live = idx < BLOCKS && r0 + 8 * rb < rtot;
 #pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    h8 x = zero_h8();
-                    if (live && gk0 + q < ktot && gr < rtot)
-                        x = load8<VEC>(X + (int64_t)(gk0 + q) * ld + gr, rtot - gr);
-                    v[p * 8 + q] = x;
+                for (int q = 0; q < 8; ++q)
+                    voff[p * 8 + q] = live ? (int)(((int64_t)(8 * kb + q) * ld + 8 * rb) * 2) : OOB_OFFSET;
+#pragma unroll
+                for (int rr = 0; rr < 8; ++rr) {
+                    int r = 8 * rb + rr;
+                    lds_off[p * 8 + rr] = idx < BLOCKS ? (r * 8 + (kb ^ swz32(r))) * 16 : -1;
                 }
             }
         }
     }
 
-    __device__ __forceinline__ void store(h8 *lds, int tid) const
+    // Loads of a step whose 64 reduction indices are all below K.
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs)
+    {
+#pragma unroll
+        for (int p = 0; p < NREG; ++p) v[p] = buffer_load16(rs, voff[p]);
+    }
+
+    // Loads of the last, partial step: reduction chunks at or beyond K read
+    // as zeros (for the transposing layouts the resource size does that).
+    __device__ __forceinline__ void load_tail(__amdgpu_buffer_rsrc_t rs, int kleft)
     {
         if constexpr (KCONT) {
 #pragma unroll
-            for (int p = 0; p < PER; ++p) {
-                int idx = tid + p * NT;
-                if (CHUNKS % NT == 0 || idx < CHUNKS) {
-                    int r = idx / KCH, c = idx % KCH;
-                    lds[r * KCH + (c ^ swz(r))] = v[p];
-                }
-            }
+            for (int p = 0; p < PER; ++p) v[p] = buffer_load16(rs, 8 * kchunk[p] < kleft ? voff[p] : OOB_OFFSET);
         } else {
-            constexpr int RB = R / 8;
+            load(rs);
+        }
+    }
+
+    __device__ __forceinline__ void store(char *lds) const
+    {
+        if constexpr (KCONT) {
+#pragma unroll
+            for (int p = 0; p < PER; ++p) *reinterpret_cast<h8 *>(lds + lds_off[p]) = v[p];
+        } else {
 #pragma unroll
             for (int p = 0; p < PER; ++p) {
-                int idx = tid + p * NT;
-                if ((CHUNKS / 8) % NT == 0 || idx < CHUNKS / 8) {
-                    int rb = idx % RB, kb = idx / RB;
+                if (BLOCKS % NT == 0 || lds_off[p * 8] >= 0) {
 #pragma unroll
                     for (int rr = 0; rr < 8; ++rr) {
                         h8 t;
 #pragma unroll
                         for (int q = 0; q < 8; ++q) t[q] = v[p * 8 + q][rr];
-                        int r = 8 * rb + rr;
-                        lds[r * KCH + (kb ^ swz(r))] = t;
+                        *reinterpret_cast<h8 *>(lds + lds_off[p * 8 + rr]) = t;
                     }
                 }
             }
@@ -178,156 +170,155 @@ struct TileCopy {
     }
 };
 
-// Map the hardware workgroup id to a (tile_m, tile_n) pair.  Workgroups are
-// dispatched round-robin over the 8 XCDs, each with its own L2, so the
-// linear order is first regrouped to give each XCD a contiguous range, and
-// that range is walked in groups of GROUP_M tile rows so the workgroups that
-// share an L2 also share A row panels and B column panels.
-__device__ __forceinline__ void tile_coords(int bid, int nwg, int tiles_m, int &tm, int &tn)
-{
-    constexpr int NXCD = 8, GROUP_M = 4;
-    int q = nwg / NXCD, rem = nwg % NXCD;
-    int xcd = bid % NXCD, local = bid / NXCD;
-    int lin = xcd < rem ? xcd * (q + 1) + local : rem * (q + 1) + (xcd - rem) * q + local;
-    int tiles_n = nwg / tiles_m;
-    int group = lin / (GROUP_M * tiles_n);
-    int first_m = group * GROUP_M;
-    int gm = tiles_m - first_m < GROUP_M ? tiles_m - first_m : GROUP_M;
-    int in_group = lin - group * GROUP_M * tiles_n;
-    tm = first_m + in_group % gm;
-    tn = in_group / gm;
-}
-
-template <int BM, int BN, int WM, int WN, int LA, int LB, bool ACC16, bool VEC>
-__global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_kernel(GemmArgs p)
+template <int BM, int BN, int WM, int WN, int LA, int LB, bool ACC16>
+__global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_fast(GemmArgs p)
 {
     constexpr int NT = 64 * WM * WN;
     constexpr int BK = 64;
-    constexpr int KCH = BK / 8;
     constexpr int WTM = BM / WM, WTN = BN / WN;
-    constexpr int TM = WTM / 16, TN = WTN / 16;
-    static_assert(WTM % 16 == 0 && WTN % 32 == 0, "wave tile: 16-row, 32-column multiples");
+    constexpr int TM = WTM / 32, TN = WTN / 32;
+    constexpr int ROWB = BK * 2;              // bytes per LDS row
+    constexpr int STAGE = (BM + BN) * ROWB;   // bytes per LDS stage
+    static_assert(WTM % 32 == 0 && WTN % 32 == 0, "warp tile must be a multiple of 32x32");
 
-    // Two stages of [A tile | B tile], in 16-byte chunks.
-    __shared__ h8 lds[2][(BM + BN) * KCH];
+    __shared__ __attribute__((aligned(16))) char lds[2 * STAGE];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int wm = wave % WM, wn = wave / WM;
+    const int l32 = lane & 31, hi = lane >> 5;
 
     int tm, tn;
     tile_coords(blockIdx.x, gridDim.x, p.tiles_m, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
 
-    TileCopy<BM, BK, NT, LA == ROW, VEC> ca;
-    TileCopy<BN, BK, NT, LB == COL, VEC> cb;
+    FastStage<BM, NT, LA == ROW> sa;
+    FastStage<BN, NT, LB == COL> sb;
+    sa.init(p.lda, m0, p.M, tid);
+    sb.init(p.ldb, n0, p.N, tid);
 
-    f4 acc[TN][TM];
+    // Resource of the step starting at reduction index k0 for each operand.
+    auto rsrc_a = [&](int k0) {
+        if constexpr (LA == ROW) return make_rsrc(p.A + (int64_t)m0 * p.lda + k0, MAX_RECORDS);
+        else return make_rsrc(p.A + (int64_t)k0 * p.lda + m0, (int64_t)(p.K - k0) * p.lda * 2);
+    };
+    auto rsrc_b = [&](int k0) {
+        if constexpr (LB == COL) return make_rsrc(p.B + (int64_t)n0 * p.ldb + k0, MAX_RECORDS);
+        else return make_rsrc(p.B + (int64_t)k0 * p.ldb + n0, (int64_t)(p.K - k0) * p.ldb * 2);
+    };
+    auto load_step = [&](int k0) {
+        if (k0 + BK <= p.K) {
+            sa.load(rsrc_a(k0));
+            sb.load(rsrc_b(k0));
+        } else {
+            sa.load_tail(rsrc_a(k0), p.K - k0);
+            sb.load_tail(rsrc_b(k0), p.K - k0);
+        }
+    };
+
+    // Fragment byte offsets inside a stage for each 16-deep slice ks; blocks
+    // further along differ by 32 rows = 4096 bytes.
+    int offq[4], offp[4];
+    {
+        const int rq = wm * WTM + l32;
+        const int rp = BM + wn * WTN + jp32(l32);
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            offq[ks] = rq * ROWB + (((2 * ks + hi) ^ swz32(l32)) * 16);
+            offp[ks] = rp * ROWB + (((2 * ks + hi) ^ swz32(jp32(l32))) * 16);
+        }
+    }
+
+    f16v acc[TN][TM];
 #pragma unroll
     for (int t = 0; t < TN; ++t)
 #pragma unroll
-        for (int s = 0; s < TM; ++s) acc[t][s] = f4{0.f, 0.f, 0.f, 0.f};
-
-    // LDS read offsets (in chunks) of this lane's fragments, before the
-    // k-chunk swizzle: row index and its swizzle value.
-    const int kq = lane >> 4;  // which 8-wide k group of a 32-deep slice
-    int rowA[TM], swA[TM], rowB[TN], swB[TN];
+        for (int s = 0; s < TM; ++s)
 #pragma unroll
-    for (int s = 0; s < TM; ++s) {
-        int r = wm * WTM + 16 * s + (lane & 15);
-        rowA[s] = r * KCH;
-        swA[s] = swz(r);
-    }
-#pragma unroll
-    for (int t = 0; t < TN; ++t) {
-        int r = wn * WTN + jperm(t, lane & 15);
-        rowB[t] = (BM + r) * KCH;
-        swB[t] = swz(r);
-    }
+            for (int e = 0; e < 16; ++e) acc[t][s][e] = 0.f;
 
     const int nk = (p.K + BK - 1) / BK;
     if (nk > 0) {
-        ca.load(p.A, p.lda, m0, 0, p.M, p.K, tid);
-        cb.load(p.B, p.ldb, n0, 0, p.N, p.K, tid);
-        ca.store(&lds[0][0], tid);
-        cb.store(&lds[0][BM * KCH], tid);
+        load_step(0);
+        sa.store(lds);
+        sb.store(lds + BM * ROWB);
         __syncthreads();
     }
 
     for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
+        char *cur = lds + (kt & 1) * STAGE;
+        char *nxt = lds + ((kt + 1) & 1) * STAGE;
         const bool more = kt + 1 < nk;
-        if (more) {
-            ca.load(p.A, p.lda, m0, (kt + 1) * BK, p.M, p.K, tid);
-            cb.load(p.B, p.ldb, n0, (kt + 1) * BK, p.N, p.K, tid);
-        }
-        const h8 *L = &lds[cur][0];
+        if (more) load_step((kt + 1) * BK);
 #pragma unroll
-        for (int ks = 0; ks < BK / 32; ++ks) {
-            const int c = ks * 4 + kq;
-            h8 fa[TM], fb[TN];
+        for (int ks = 0; ks < 4; ++ks) {
+            h8 fq[TM], fp[TN];
 #pragma unroll
-            for (int s = 0; s < TM; ++s) fa[s] = L[rowA[s] + (c ^ swA[s])];
+            for (int s = 0; s < TM; ++s) fq[s] = *reinterpret_cast<const h8 *>(cur + offq[ks] + s * 32 * ROWB);
 #pragma unroll
-            for (int t = 0; t < TN; ++t) fb[t] = L[rowB[t] + (c ^ swB[t])];
+            for (int t = 0; t < TN; ++t) fp[t] = *reinterpret_cast<const h8 *>(cur + offp[ks] + t * 32 * ROWB);
 #pragma unroll
             for (int t = 0; t < TN; ++t)
 #pragma unroll
                 for (int s = 0; s < TM; ++s)
-                    acc[t][s] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fb[t], fa[s], acc[t][s], 0, 0, 0);
+                    acc[t][s] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fp[t], fq[s], acc[t][s], 0, 0, 0);
             if constexpr (ACC16) {
-                // fp16 accumulation: the running sum is rounded to fp16 at
-                // the end of every aligned 32-deep group of k.
+                if (ks & 1) {
+                    // fp16 accumulation: round the running sum to fp16 at the
+                    // end of every aligned 32-deep group of k.
 #pragma unroll
-                for (int t = 0; t < TN; ++t)
+                    for (int t = 0; t < TN; ++t)
 #pragma unroll
-                    for (int s = 0; s < TM; ++s)
+                        for (int s = 0; s < TM; ++s)
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) acc[t][s][e] = (float)(_Float16)acc[t][s][e];
+                            for (int e = 0; e < 16; ++e) acc[t][s][e] = (float)(_Float16)acc[t][s][e];
+                }
             }
         }
         if (more) {
-            ca.store(&lds[cur ^ 1][0], tid);
-            cb.store(&lds[cur ^ 1][BM * KCH], tid);
+            sa.store(nxt);
+            sb.store(nxt + BM * ROWB);
         }
         __syncthreads();
     }
 
-    // Epilogue on registers: + bias, ReLU, fp16, one 16-byte store per lane
-    // per pair of MFMA blocks.
+    // Epilogue on registers: + bias, ReLU, fp16, two 16-byte stores per lane
+    // per 32x32 block.
 #pragma unroll
-    for (int pr = 0; pr < TN / 2; ++pr) {
-        const int j = n0 + wn * WTN + 32 * pr + 8 * kq;
-        float b[8];
-        if (p.bias != nullptr) {
-            h8 bv = zero_h8();
-            if (j < p.N) bv = load8<VEC>(p.bias + j, p.N - j);
+    for (int t = 0; t < TN; ++t) {
+        const int j = n0 + wn * WTN + 32 * t + 16 * hi;
+        float b[16];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) b[e] = (float)bv[e];
-        } else {
+        for (int e = 0; e < 16; ++e) b[e] = 0.f;
+        if (p.bias != nullptr && j < p.N) {
+            h8 b0 = *reinterpret_cast<const h8 *>(p.bias + j);
+            h8 b1 = j + 8 < p.N ? *reinterpret_cast<const h8 *>(p.bias + j + 8) : zero_h8();
 #pragma unroll
-            for (int e = 0; e < 8; ++e) b[e] = 0.f;
+            for (int e = 0; e < 8; ++e) {
+                b[e] = (float)b0[e];
+                b[8 + e] = (float)b1[e];
+            }
         }
 #pragma unroll
         for (int s = 0; s < TM; ++s) {
-            const int i = m0 + wm * WTM + 16 * s + (lane & 15);
-            h8 o;
+            const int i = m0 + wm * WTM + 32 * s + l32;
+            h8 o0, o1;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                float x = (e < 4 ? acc[2 * pr][s][e] : acc[2 * pr + 1][s][e - 4]) + b[e];
-                if (p.relu) x = x > 0.f ? x : 0.f;
-                o[e] = (_Float16)x;
+                float x0 = acc[t][s][e] + b[e];
+                float x1 = acc[t][s][8 + e] + b[8 + e];
+                if (p.relu) {
+                    x0 = x0 > 0.f ? x0 : 0.f;
+                    x1 = x1 > 0.f ? x1 : 0.f;
+                }
+                o0[e] = (_Float16)x0;
+                o1[e] = (_Float16)x1;
             }
             if (i < p.M && j < p.N) {
                 _Float16 *dst = p.C + (int64_t)i * p.ldc + j;
-                if (VEC && j + 8 <= p.N) {
-                    *reinterpret_cast<h8 *>(dst) = o;
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        if (j + e < p.N) dst[e] = o[e];
-                }
+                *reinterpret_cast<h8 *>(dst) = o0;
+                if (j + 8 < p.N) *reinterpret_cast<h8 *>(dst + 8) = o1;
             }
         }
     }

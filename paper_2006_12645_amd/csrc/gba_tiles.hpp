@@ -6,12 +6,13 @@
 // best per problem size (Experimental Evaluation section); this table is the
 // MI355X counterpart of that tile space.  Block tiles are sized for the
 // 160 KB LDS of a gfx950 compute unit (two stages of (BM + BN) x 64 fp16)
-// and wave tiles for its 512 registers per lane.
+// and warp tiles for its 512 registers per lane.
 #pragma once
 
 #include <hip/hip_runtime.h>
 
 #include "gba_kernel.hpp"
+#include "gba_kernel_generic.hpp"
 
 namespace gba {
 
@@ -20,40 +21,53 @@ struct TileCfg {
 };
 
 // X(id, BM, BN, WM, WN): BM output rows x BN output columns per workgroup,
-// WM x WN waves, each owning a (BM/WM) x (BN/WN) sub-tile.
+// WM x WN waves, each owning a (BM/WM) x (BN/WN) warp tile (multiples of
+// 32 x 32, the MFMA block).
 #define GBA_TILE_LIST(X)   \
-    X(0, 256, 256, 2, 4)   \
-    X(1, 256, 256, 2, 2)   \
-    X(2, 128, 128, 2, 2)   \
-    X(3, 256, 128, 2, 2)   \
-    X(4, 128, 256, 2, 2)   \
-    X(5, 64, 64, 2, 2)     \
-    X(6, 32, 64, 1, 2)     \
-    X(7, 64, 128, 2, 2)
+    X(0, 256, 256, 2, 2)   \
+    X(1, 256, 256, 2, 4)   \
+    X(2, 256, 128, 2, 2)   \
+    X(3, 128, 256, 2, 2)   \
+    X(4, 128, 128, 2, 2)   \
+    X(5, 128, 64, 2, 2)    \
+    X(6, 64, 64, 2, 2)     \
+    X(7, 64, 128, 2, 2)    \
+    X(8, 32, 64, 1, 2)     \
+    X(9, 32, 32, 1, 1)
 
-constexpr int NUM_TILES = 8;
-// The configuration used whenever an operand is not 16-byte aligned.
-constexpr int GENERIC_TILE = 5;
+constexpr int NUM_TILES = 10;
 
 #define GBA_TILE_CFG(id, BM, BN, WM, WN) TileCfg{BM, BN, WM, WN},
 constexpr TileCfg TILES[NUM_TILES] = {GBA_TILE_LIST(GBA_TILE_CFG)};
 #undef GBA_TILE_CFG
 
+// Block tile of the general path (any size, leading dimension, alignment).
+constexpr TileCfg GENERIC_TILE = {64, 64, 2, 2};
+
 typedef hipError_t (*LaunchFn)(const GemmArgs &, hipStream_t);
 
-// Per operand-layout pair: vec[tile][acc16] for 16-byte aligned operands,
-// scalar[acc16] (GENERIC_TILE) otherwise.
+// Per operand-layout pair: fast[tile][acc16] for the aligned fast path,
+// generic[acc16] otherwise.
 struct LayoutTable {
-    LaunchFn vec[NUM_TILES][2];
-    LaunchFn scalar[2];
+    LaunchFn fast[NUM_TILES][2];
+    LaunchFn generic[2];
 };
 
-template <int BM, int BN, int WM, int WN, int LA, int LB, bool ACC16, bool VEC>
-hipError_t launch_gemm(const GemmArgs &a, hipStream_t s)
+template <int BM, int BN, int WM, int WN, int LA, int LB, bool ACC16>
+hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
 {
     dim3 grid((unsigned)(a.tiles_m * a.tiles_n)), block(64 * WM * WN);
-    hipLaunchKernelGGL((gemm_bias_act_kernel<BM, BN, WM, WN, LA, LB, ACC16, VEC>), grid, block, 0,
-                       s, a);
+    hipLaunchKernelGGL((gemm_bias_act_fast<BM, BN, WM, WN, LA, LB, ACC16>), grid, block, 0, s, a);
+    return hipGetLastError();
+}
+
+template <int LA, int LB, bool ACC16>
+hipError_t launch_generic(const GemmArgs &a, hipStream_t s)
+{
+    constexpr TileCfg c = GENERIC_TILE;
+    dim3 grid((unsigned)(a.tiles_m * a.tiles_n)), block(64 * c.wm * c.wn);
+    hipLaunchKernelGGL((gemm_bias_act_generic<c.bm, c.bn, c.wm, c.wn, LA, LB, ACC16, false>), grid,
+                       block, 0, s, a);
     return hipGetLastError();
 }
 

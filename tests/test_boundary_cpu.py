@@ -60,7 +60,7 @@ def gemm(M=64, N=64, K=64, la=0, lb=1, A=FAKE, lda=None, B=FAKE, ldb=None, bias=
     (dict(A=None), gba.GBA_EINVAL),
     (dict(B=None), gba.GBA_EINVAL),
     (dict(C=None), gba.GBA_EINVAL),
-    (dict(tile=8), gba.GBA_EINVAL),
+    (dict(tile=10), gba.GBA_EINVAL),
     (dict(tile=1000), gba.GBA_EINVAL),
     (dict(A=FAKE + 1), gba.GBA_EUNSUPPORTED),
     (dict(C=FAKE + 1), gba.GBA_EUNSUPPORTED),

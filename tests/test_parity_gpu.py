@@ -17,6 +17,7 @@ torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
 LAYOUTS = ["RR", "RC", "CR", "CC"]
+NUM_TILES = 10
 
 
 def announce(*what):
@@ -160,19 +161,24 @@ def test_integer_data_bit_exact(layout, accum):
     assert np.array_equal(got, U.oracle_for(A, B, bias))
 
 
-@pytest.mark.parametrize("tile", range(8))
+def test_tile_count():
+    assert gba.num_tiles() == NUM_TILES
+
+
+@pytest.mark.parametrize("tile", range(NUM_TILES))
 @pytest.mark.parametrize("layout", LAYOUTS)
 def test_every_tile_config(tile, layout):
-    M, N, K = 300, 330, 200
+    """Fast path (sizes multiples of 8, ragged against every tile)."""
+    M, N, K = 296, 328, 200
     announce("tile", tile, layout)
     A, B, bias = D.random_problem(1000 + tile, M, N, K)
     got = run_gpu(A, B, bias, layout, tile=tile).cpu().numpy()
     U.assert_close(got, U.oracle_for(A, B, bias), what=f"tile {tile} {layout}")
 
 
-@pytest.mark.parametrize("tile", range(8))
+@pytest.mark.parametrize("tile", range(NUM_TILES))
 def test_every_tile_config_f16acc(tile):
-    M, N, K = 130, 250, 515
+    M, N, K = 136, 248, 520
     announce("tile f16acc", tile)
     A, B, bias = D.random_problem(1100 + tile, M, N, K)
     got = run_gpu(A, B, bias, "RC", accum="f16", tile=tile).cpu().numpy()
