@@ -100,12 +100,28 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--workload", default=HEADLINE)
     ap.add_argument("--tile", type=int, default=None)
     ap.add_argument("--report", default=None, help="also write per-variant numbers here (JSON)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--fused-only", action="store_true",
+                    help="time only the fused kernel (for profiler runs); implies --no-cpu")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run 5 plain device-to-device copies of MIB MiB (the reference "
+                         "kernel for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE) and exit")
     args = ap.parse_args()
+
+    if args.calibrate_copy:
+        import torch
+        n = args.calibrate_copy * (1 << 20)
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_per_launch": n, "launches": 5}), flush=True)
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the fused kernel has no multi-GPU path; "
@@ -134,9 +150,15 @@ def main():
     torch.cuda.synchronize()
     ms = time_launches(fused, args.steps, args.warmup, torch)
     torch.cuda.synchronize()
-    ms_plain = time_launches(plain, args.steps, args.warmup, torch)
-    ms_unfused = time_launches(unfused, args.steps, args.warmup, torch)
-    ms_fused2 = time_launches(fused, args.steps, args.warmup, torch)
+    if args.fused_only:
+        args.no_cpu = True
+        ms_plain = ms_unfused = ms_fused2 = float("nan")
+    else:
+        # the comparison legs get the same warmup, then the fused kernel is
+        # timed once more right after the unfused chain
+        ms_plain = time_launches(plain, args.steps, args.warmup, torch)
+        ms_unfused = time_launches(unfused, args.steps, args.warmup, torch)
+        ms_fused2 = time_launches(fused, args.steps, 0, torch)
 
     flops = 2.0 * w.M * w.N * w.K
     tflops = flops / (ms * 1e-3) / 1e12
@@ -169,7 +191,7 @@ def main():
                      "unit": "TFLOP/s", "frac": round(tflops / PEAK_F16_TFLOPS, 4),
                      "traffic": traffic},
         "cpu_baseline": cpu,
-        "extra": {
+        "extra": None if args.fused_only else {
             "frac_of_fp16_peak": round(tflops / PEAK_F16_TFLOPS, 4),
             "fused_ms_second_pass": round(ms_fused2, 5),
             "plain_gemm_ms": round(ms_plain, 5),

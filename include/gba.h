@@ -88,8 +88,11 @@ gba_status gemm_bias_act(gba_layout layoutA, gba_layout layoutB,
  * the fastest per problem size (Experimental Evaluation section); this entry
  * point exposes that choice for sweeps.  tile_id indexes the table reported
  * by gba_tile_info; tile_id < 0 means "let the library choose" (identical to
- * gemm_bias_act).  Errors as gemm_bias_act, plus GBA_EINVAL for a tile_id at
- * or beyond gba_num_tiles().
+ * gemm_bias_act).  A tile larger than the problem (bm > M or bn > N) is
+ * replaced by the library's choice, and operands that miss the fast path's
+ * alignment conditions use the general kernel whatever tile_id says.  Errors
+ * as gemm_bias_act, plus GBA_EINVAL for a tile_id at or beyond
+ * gba_num_tiles().
  */
 gba_status gemm_bias_act_tile(gba_layout layoutA, gba_layout layoutB,
                               int64_t M, int64_t N, int64_t K,
@@ -113,8 +116,9 @@ gba_status gba_tile_info(int tile_id, int *bm, int *bn, int *bk, int *waves, int
 
 /*
  * gba_select_tile -- the tile configuration gemm_bias_act would use for this
- * problem (host-only computation, no GPU access).  Returns the tile id, or
- * -1 if the arguments are invalid.
+ * problem on its aligned fast path (host-only computation, no GPU access).
+ * Returns the tile id, or -1 if the arguments are invalid or the problem is
+ * smaller than every tile (M < 32 or N < 32: general path).
  */
 int gba_select_tile(gba_layout layoutA, gba_layout layoutB, int64_t M, int64_t N, int64_t K,
                     gba_acc accum);

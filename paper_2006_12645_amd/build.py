@@ -58,8 +58,20 @@ def build(verbose: bool = False) -> str:
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
+    _check_no_missing_kernels(tmp)
     os.replace(tmp, LIB)
     return LIB
+
+
+def _check_no_missing_kernels(lib):
+    """Fail the build if any kernel launch stub is left undefined (a kernel
+    the host pass silently did not instantiate)."""
+    r = subprocess.run(["nm", "-D", "--undefined-only", lib], capture_output=True, text=True)
+    if r.returncode != 0:
+        return  # nm unavailable: the loader will report it instead
+    missing = [l.split()[-1] for l in r.stdout.splitlines() if "__device_stub__" in l]
+    if missing:
+        raise RuntimeError(f"{len(missing)} kernel stubs undefined in {lib}, e.g. {missing[0]}")
 
 
 if __name__ == "__main__":

@@ -37,20 +37,21 @@ gba_status validate_gemm(int la, int lb, int64_t M, int64_t N, int64_t K, const 
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// Tile choice by problem shape: the largest block tile that still yields
-// enough workgroups to occupy the 256 compute units.
+bool tile_fits(int tile, int64_t M, int64_t N) { return M >= TILES[tile].bm && N >= TILES[tile].bn; }
+
+// Tile choice by problem shape: the largest block tile that fits inside the
+// problem and still yields enough workgroups to occupy the 256 compute
+// units; failing that, the one with the most workgroups.
 int select_tile(int64_t M, int64_t N, int64_t K)
 {
     (void)K;
     const int64_t CUS = 256;
-    if (ceil_div(M, 256) * ceil_div(N, 256) >= CUS) return 0;
-    if (ceil_div(M, 256) * ceil_div(N, 128) >= CUS) return 2;
-    if (ceil_div(M, 128) * ceil_div(N, 256) >= CUS) return 3;
-    if (ceil_div(M, 128) * ceil_div(N, 128) >= CUS) return 4;
-    if (ceil_div(M, 128) * ceil_div(N, 64) >= CUS) return 5;
-    if (ceil_div(M, 64) * ceil_div(N, 64) >= CUS) return 6;
-    if (M <= 32) return N >= 4096 ? 8 : 9;
-    return 6;
+    static const int order[] = {1, 2, 3, 4, 5, 7, 6, 8, 9};
+    for (int t : order)
+        if (tile_fits(t, M, N) && ceil_div(M, TILES[t].bm) * ceil_div(N, TILES[t].bn) >= CUS) return t;
+    for (int t : {6, 8, 9})
+        if (tile_fits(t, M, N)) return t;
+    return -1;  // smaller than the smallest tile: general path
 }
 
 // Largest leading dimension the fast path addresses with 32-bit offsets.
@@ -83,8 +84,11 @@ gba_status run_gemm(int la, int lb, int64_t M, int64_t N, int64_t K, const void 
     gba_status st = validate_gemm(la, lb, M, N, K, A, lda, B, ldb, bias, C, ldc, act, accum);
     if (st != GBA_OK || M == 0 || N == 0) return st;
 
-    const bool fast = fast_path_ok(la, lb, M, N, K, A, lda, B, ldb, bias, C, ldc);
-    const int tile = fast ? (tile_id >= 0 ? tile_id : select_tile(M, N, K)) : -1;
+    // A requested tile that is larger than the problem is replaced by the
+    // library's choice; problems smaller than every tile take the general path.
+    int tile = tile_id >= 0 && tile_fits(tile_id, M, N) ? tile_id : select_tile(M, N, K);
+    const bool fast = tile >= 0 && fast_path_ok(la, lb, M, N, K, A, lda, B, ldb, bias, C, ldc);
+    if (!fast) tile = -1;
     const TileCfg cfg = fast ? TILES[tile] : GENERIC_TILE;
 
     GemmArgs a;
@@ -221,7 +225,7 @@ extern "C" int gba_select_tile(gba_layout layoutA, gba_layout layoutB, int64_t M
     if (!is_layout(layoutA) || !is_layout(layoutB)) return -1;
     if (accum != GBA_ACC_F32 && accum != GBA_ACC_F16) return -1;
     if (M < 0 || N < 0 || K < 0 || M > INT_MAX || N > INT_MAX || K > INT_MAX) return -1;
-    return select_tile(M, N, K);
+    return select_tile(M, N, K);  // -1 also when the general path would run
 }
 
 extern "C" gba_status gba_bias_add_f16(int64_t M, int64_t N, void *C, int64_t ldc, const void *bias,

@@ -43,10 +43,15 @@
 // block of fp16 as 8 chunks along M (or N), transposes it in registers and
 // writes 8 reduction-contiguous chunks: the per-layout copy helpers.
 //
-// Edges.  Out-of-range chunks are fetched through a buffer resource with an
-// offset beyond its size, which the hardware returns as zeros without a
-// branch; out-of-range outputs are not stored.
+// Edges.  A tile that would cross the last row or column of C is shifted
+// back inside the matrix (this path needs M >= BM and N >= BN), so its loads
+// never leave the operands; the outputs it shares with its neighbour are
+// stored only by the tile that owns them.  Reduction indices at or beyond K
+// (last step only) are fetched through a buffer offset beyond the resource's
+// size, which the hardware returns as zeros without a branch.
 #pragma once
+
+#include <type_traits>
 
 #include "gba_common.hpp"
 
@@ -64,11 +69,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const _Float16 *base
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<_Float16 *>(base), (short)0, n, RSRC_WORD3);
 }
 
-__device__ __forceinline__ h8 buffer_load16(__amdgpu_buffer_rsrc_t r, int voff)
-{
-    return __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
-}
-
 // Chunk permutation of LDS row r (periodic in 32 rows).
 __device__ __forceinline__ int swz32(int r)
 {
@@ -83,86 +83,101 @@ __device__ __forceinline__ int swz32(int r)
 // lane, which this maps to column 16*(lane/32) + r.
 __device__ __forceinline__ int jp32(int rho) { return 16 * ((rho >> 2) & 1) + 4 * (rho >> 3) + (rho & 3); }
 
+__device__ __forceinline__ h8 buffer_load16(__amdgpu_buffer_rsrc_t r, int voff, int soff)
+{
+    return __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
 // One operand tile of R rows (output rows of A, or output columns of B) by
-// 64 reduction indices: per-thread chunk offsets, staging registers, and the
-// register -> LDS write.
-//   KCONT: reduction-contiguous in global memory (row-major A, col-major B).
+// 64 reduction indices: the staging registers and the global -> register and
+// register -> LDS copies.  The tile origin is always inside the matrix and
+// the tile never extends past its last row (edge tiles are shifted back), so
+// every chunk address is one per-lane offset plus a per-chunk scalar offset.
+// Only reduction indices at or beyond K must read as zero: the per-lane
+// offset of such a chunk is replaced by OOB_OFFSET.
+//   KCONT: reduction-contiguous in global memory (row-major A, col-major B):
+//          lane t copies chunk t%8 of rows t/8 + (NT/8)*p.
+//   otherwise: lane t copies the 8 x 8 block (reduction rows 8*kb..8*kb+7,
+//          tile rows 8*rb..8*rb+7), rb = idx % (R/8), kb = idx / (R/8),
+//          idx = t + NT*p, and transposes it in registers.
 template <int R, int NT, bool KCONT>
 struct FastStage {
-    static constexpr int CHUNKS = R * 8;
-    static constexpr int BLOCKS = R;  // 8 x 8 blocks when transposing
-    static constexpr int PER = KCONT ? CHUNKS / NT : (BLOCKS + NT - 1) / NT;
+    static constexpr int RB = R / 8;                    // 8-row groups of the tile
+    static constexpr int PER = KCONT ? R * 8 / NT : (R + NT - 1) / NT;
     static constexpr int NREG = KCONT ? PER : PER * 8;
-    static_assert(!KCONT || CHUNKS % NT == 0, "chunks must divide evenly among the threads");
+    static constexpr bool PARTIAL = !KCONT && R % NT != 0;  // some lanes idle
+    static_assert(!KCONT || (R * 8) % NT == 0, "chunks must divide evenly among the threads");
+    static_assert(KCONT || NT % RB == 0 || R < NT, "blocks must tile the threads");
 
-    int voff[NREG];      // byte offset of each chunk from the tile origin (or OOB_OFFSET)
-    int kchunk[KCONT ? PER : 1];  // reduction chunk index (KCONT tail masking)
-    int lds_off[KCONT ? PER : PER * 8];  // LDS byte offset of each written chunk
+    int voff;        // byte offset of the lane's first chunk from the step origin
+    int lds0;        // KCONT: LDS byte offset of the lane's first chunk
+    int ldsr[KCONT ? 1 : PER * 8];  // transposing: LDS byte offset of each written row
+    int kq;          // reduction offset (elements) of the lane's first chunk
+    bool live;       // transposing: this lane owns a block
+    int64_t ldb2;    // leading dimension in bytes
     h8 v[NREG];
 
-    __device__ __forceinline__ void init(int64_t ld, int r0, int rtot, int tid)
+    __device__ __forceinline__ void init(int64_t ld, int tid)
     {
+        ldb2 = ld * 2;
         if constexpr (KCONT) {
-#pragma unroll
-            for (int p = 0; p < PER; ++p) {
-                int idx = tid + p * NT;
-                int r = idx >> 3, c = idx & 7;
-                voff[p] = r0 + r < rtot ? (int)(((int64_t)r * ld + 8 * c) * 2) : OOB_OFFSET;
-                kchunk[p] = c;
-                lds_off[p] = (r * 8 + (c ^ swz32(r))) * 16;
-            }
+            const int r = tid >> 3, c = tid & 7;
+            voff = (int)(r * ldb2) + 16 * c;
+            lds0 = (r * 8 + (c ^ swz32(r))) * 16;
+            kq = 8 * c;
+            live = true;
         } else {
+            const int rb = tid % RB, kb = tid / RB;
+            live = tid < R;
+            voff = (int)(8 * kb * ldb2) + 16 * rb;
+            kq = 8 * kb;
 #pragma unroll
-            for (int p = 0; p < PER; ++p) {
-                int idx = tid + p * NT;
-                int rb = idx % (R / 8), kb = idx / (R / 8);
-                bool live = idx < BLOCKS && r0 + 8 * rb < rtot;
-#pragma unroll
-                for (int q = 0; q < 8; ++q)
-                    voff[p * 8 + q] = live ? (int)(((int64_t)(8 * kb + q) * ld + 8 * rb) * 2) : OOB_OFFSET;
+            for (int p = 0; p < PER; ++p)
 #pragma unroll
                 for (int rr = 0; rr < 8; ++rr) {
-                    int r = 8 * rb + rr;
-                    lds_off[p * 8 + rr] = idx < BLOCKS ? (r * 8 + (kb ^ swz32(r))) * 16 : -1;
+                    const int r = 8 * rb + rr;
+                    ldsr[p * 8 + rr] = (r * 8 + ((kb + p * (NT / RB)) ^ swz32(r))) * 16;
                 }
-            }
         }
     }
 
-    // Loads of a step whose 64 reduction indices are all below K.
-    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs)
+    // Scalar byte offset of staging register i.
+    __device__ __forceinline__ int soff(int i) const
     {
-#pragma unroll
-        for (int p = 0; p < NREG; ++p) v[p] = buffer_load16(rs, voff[p]);
+        if constexpr (KCONT) return (int)(i * (NT / 8) * ldb2);
+        else return (int)(((i / 8) * (NT / RB) * 8 + (i % 8)) * ldb2);
+    }
+    // Reduction index (relative to the step) of staging register i's chunk.
+    __device__ __forceinline__ int kidx(int i) const
+    {
+        if constexpr (KCONT) return kq;
+        else return kq + (i / 8) * (NT / RB) * 8 + (i % 8);
     }
 
-    // Loads of the last, partial step: reduction chunks at or beyond K read
-    // as zeros (for the transposing layouts the resource size does that).
-    __device__ __forceinline__ void load_tail(__amdgpu_buffer_rsrc_t rs, int kleft)
+    // Loads of one step; chunks at or beyond kleft (= K - step origin) read
+    // as zero.
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, int kleft)
     {
-        if constexpr (KCONT) {
 #pragma unroll
-            for (int p = 0; p < PER; ++p) v[p] = buffer_load16(rs, 8 * kchunk[p] < kleft ? voff[p] : OOB_OFFSET);
-        } else {
-            load(rs);
-        }
+        for (int i = 0; i < NREG; ++i) v[i] = buffer_load16(rs, kidx(i) < kleft ? voff : OOB_OFFSET, soff(i));
     }
 
     __device__ __forceinline__ void store(char *lds) const
     {
         if constexpr (KCONT) {
 #pragma unroll
-            for (int p = 0; p < PER; ++p) *reinterpret_cast<h8 *>(lds + lds_off[p]) = v[p];
+            for (int p = 0; p < PER; ++p)
+                *reinterpret_cast<h8 *>(lds + lds0 + p * (NT / 8) * 128) = v[p];
         } else {
 #pragma unroll
             for (int p = 0; p < PER; ++p) {
-                if (BLOCKS % NT == 0 || lds_off[p * 8] >= 0) {
+                if (!PARTIAL || live) {
 #pragma unroll
                     for (int rr = 0; rr < 8; ++rr) {
                         h8 t;
 #pragma unroll
                         for (int q = 0; q < 8; ++q) t[q] = v[p * 8 + q][rr];
-                        *reinterpret_cast<h8 *>(lds + lds_off[p * 8 + rr]) = t;
+                        *reinterpret_cast<h8 *>(lds + ldsr[p * 8 + rr]) = t;
                     }
                 }
             }
@@ -170,7 +185,95 @@ struct FastStage {
     }
 };
 
-template <int BM, int BN, int WM, int WN, int LA, int LB, bool ACC16>
+typedef __attribute__((address_space(3))) void lds_void;
+
+// 16 bytes per lane from buffer `rs` straight into LDS at `lds` + 16 * lane.
+__device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t rs, char *lds, int voff, int soff)
+{
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)lds, 16, voff, soff, 0, 0);
+}
+
+// Scheduling hints for one 16-deep slice of NM MFMAs: the NR fragment reads
+// for the next slice go first (so they have the whole slice to land), then
+// half of the MFMAs, then the CNT instructions of class MASK (staging writes
+// 0x200 or global copies 0x020), then the other half of the MFMAs.
+template <int NM, int NR, int MASK, int CNT>
+__device__ __forceinline__ void sched_slice()
+{
+    __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, NM / 2, 0);
+    if constexpr (CNT > 0) __builtin_amdgcn_sched_group_barrier(MASK, CNT, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, NM - NM / 2, 0);
+}
+
+// Register-staged copy of one operand tile (any layout): global -> registers
+// during one step, registers -> LDS during the next.
+template <int R, int NT, bool KCONT>
+struct RegCopy {
+    using Stage = FastStage<R, NT, KCONT>;
+    static constexpr int NLOAD = Stage::NREG;                   // global loads per step
+    static constexpr int NWRITE = KCONT ? Stage::PER : Stage::PER * 8;  // LDS writes per step
+    Stage st;
+    __device__ __forceinline__ void init(int64_t ld, int tid) { st.init(ld, tid); }
+    __device__ __forceinline__ void dma(__amdgpu_buffer_rsrc_t, char *, int) {}
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, int kleft) { st.load(rs, kleft); }
+    __device__ __forceinline__ void write(char *stage) const { st.store(stage); }
+};
+
+// Direct global -> LDS copy of a reduction-contiguous operand tile with the
+// gfx950 buffer_load_dwordx4 ... lds form: each instruction moves 64 chunks
+// of 16 bytes into 1 KB of LDS in lane order (8 rows of 128 bytes), so lane
+// l fetches the global chunk that the swizzle places at position l % 8 of
+// row l / 8.  No registers hold the data and no LDS write instruction is
+// issued.  Instruction i of wave w fills rows 8*(NW*i + w) .. +7.  A chunk
+// at or beyond K is fetched with an out-of-range offset, for which the copy
+// writes zeros.
+template <int R, int NT>
+struct DmaCopy {
+    static constexpr int NW = NT / 64;
+    static constexpr int NI = R / (8 * NW);                   // instructions per wave per step
+    static constexpr int NV0 = (8 * NW) % 32 == 0 ? 1 : 32 / (8 * NW);
+    static constexpr int NV = NV0 < NI ? NV0 : NI;            // distinct lane offsets
+    static constexpr int NLOAD = NI;
+    static constexpr int NWRITE = 0;
+    static_assert(R % (8 * NW) == 0, "rows must divide evenly among the waves");
+
+    int voff[NV];  // lane byte offset from the instruction's first row
+    int kq[NV];    // reduction index of the lane's chunk
+    int w;         // wave index (uniform)
+    int64_t ldb2;
+
+    __device__ __forceinline__ void init(int64_t ld, int tid)
+    {
+        ldb2 = ld * 2;
+        w = __builtin_amdgcn_readfirstlane(tid >> 6);
+        const int l = tid & 63;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            const int row = 8 * (NW * v + w) + (l >> 3);
+            const int c = (l & 7) ^ swz32(row);
+            voff[v] = (int)((l >> 3) * ldb2) + 16 * c;
+            kq[v] = 8 * c;
+        }
+    }
+
+    // Issue the step's copies into `stage`; chunks at or beyond kleft
+    // (= K - step origin) become zeros.
+    __device__ __forceinline__ void dma(__amdgpu_buffer_rsrc_t rs, char *stage, int kleft)
+    {
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int v = i % NV;
+            const int row0 = 8 * (NW * i + w);
+            buffer_load16_lds(rs, stage + row0 * 128, kq[v] < kleft ? voff[v] : OOB_OFFSET,
+                              (int)(row0 * ldb2));
+        }
+    }
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t, int) {}
+    __device__ __forceinline__ void write(char *) const {}
+};
+
+template <int BM, int BN, int WM, int WN, int LA, int LB, bool ACC16, bool DMA>
 __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_fast(GemmArgs p)
 {
     constexpr int NT = 64 * WM * WN;
@@ -191,30 +294,45 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_fast(GemmArgs p)
 
     int tm, tn;
     tile_coords(blockIdx.x, gridDim.x, p.tiles_m, tm, tn);
+    // Output tile origin, and the origin of the tile actually computed: an
+    // edge tile is shifted back so that it lies inside the matrix (M >= BM
+    // and N >= BN on this path); the rows/columns it shares with its
+    // neighbour are computed twice but stored once.
     const int m0 = tm * BM, n0 = tn * BN;
+    const int mc = m0 + BM <= p.M ? m0 : p.M - BM;
+    const int nc = n0 + BN <= p.N ? n0 : p.N - BN;
 
-    FastStage<BM, NT, LA == ROW> sa;
-    FastStage<BN, NT, LB == COL> sb;
-    sa.init(p.lda, m0, p.M, tid);
-    sb.init(p.ldb, n0, p.N, tid);
+    using CopyA = std::conditional_t<DMA && LA == ROW, DmaCopy<BM, NT>, RegCopy<BM, NT, LA == ROW>>;
+    using CopyB = std::conditional_t<DMA && LB == COL, DmaCopy<BN, NT>, RegCopy<BN, NT, LB == COL>>;
+    CopyA ca;
+    CopyB cb;
+    ca.init(p.lda, tid);
+    cb.init(p.ldb, tid);
 
     // Resource of the step starting at reduction index k0 for each operand.
     auto rsrc_a = [&](int k0) {
-        if constexpr (LA == ROW) return make_rsrc(p.A + (int64_t)m0 * p.lda + k0, MAX_RECORDS);
-        else return make_rsrc(p.A + (int64_t)k0 * p.lda + m0, (int64_t)(p.K - k0) * p.lda * 2);
+        if constexpr (LA == ROW) return make_rsrc(p.A + (int64_t)mc * p.lda + k0, MAX_RECORDS);
+        else return make_rsrc(p.A + (int64_t)k0 * p.lda + mc, MAX_RECORDS);
     };
     auto rsrc_b = [&](int k0) {
-        if constexpr (LB == COL) return make_rsrc(p.B + (int64_t)n0 * p.ldb + k0, MAX_RECORDS);
-        else return make_rsrc(p.B + (int64_t)k0 * p.ldb + n0, (int64_t)(p.K - k0) * p.ldb * 2);
+        if constexpr (LB == COL) return make_rsrc(p.B + (int64_t)nc * p.ldb + k0, MAX_RECORDS);
+        else return make_rsrc(p.B + (int64_t)k0 * p.ldb + nc, MAX_RECORDS);
     };
-    auto load_step = [&](int k0) {
-        if (k0 + BK <= p.K) {
-            sa.load(rsrc_a(k0));
-            sb.load(rsrc_b(k0));
-        } else {
-            sa.load_tail(rsrc_a(k0), p.K - k0);
-            sb.load_tail(rsrc_b(k0), p.K - k0);
-        }
+    const int nk = (p.K + BK - 1) / BK;
+
+    // Copies of step s: direct-to-LDS operands into `stage`, the others into
+    // their staging registers.  Steps past the last one re-fetch the last
+    // step (into a stage nobody reads again), so every step of the loop
+    // below has the same shape.
+    auto copy_step = [&](int s, char *stage) {
+        const int k0 = (s < nk ? s : nk - 1) * BK;
+        const int kleft = p.K - k0;
+        const auto ra = rsrc_a(k0);
+        const auto rb = rsrc_b(k0);
+        ca.dma(ra, stage, kleft);
+        cb.dma(rb, stage + BM * ROWB, kleft);
+        ca.load(ra, kleft);
+        cb.load(rb, kleft);
     };
 
     // Fragment byte offsets inside a stage for each 16-deep slice ks; blocks
@@ -238,71 +356,109 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_fast(GemmArgs p)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[t][s][e] = 0.f;
 
-    const int nk = (p.K + BK - 1) / BK;
-    if (nk > 0) {
-        load_step(0);
-        sa.store(lds);
-        sb.store(lds + BM * ROWB);
-        __syncthreads();
-    }
-
-    for (int kt = 0; kt < nk; ++kt) {
-        char *cur = lds + (kt & 1) * STAGE;
-        char *nxt = lds + ((kt + 1) & 1) * STAGE;
-        const bool more = kt + 1 < nk;
-        if (more) load_step((kt + 1) * BK);
+    // Fragments of two 16-deep slices: one being multiplied, one in flight.
+    h8 fq[2][TM], fp[2][TN];
+    auto read_frags = [&](int buf, const char *stage, int ks) {
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            h8 fq[TM], fp[TN];
+        for (int s = 0; s < TM; ++s) fq[buf][s] = *reinterpret_cast<const h8 *>(stage + offq[ks] + s * 32 * ROWB);
 #pragma unroll
-            for (int s = 0; s < TM; ++s) fq[s] = *reinterpret_cast<const h8 *>(cur + offq[ks] + s * 32 * ROWB);
+        for (int t = 0; t < TN; ++t) fp[buf][t] = *reinterpret_cast<const h8 *>(stage + offp[ks] + t * 32 * ROWB);
+    };
+    auto mfmas = [&](int buf) {
 #pragma unroll
-            for (int t = 0; t < TN; ++t) fp[t] = *reinterpret_cast<const h8 *>(cur + offp[ks] + t * 32 * ROWB);
+        for (int t = 0; t < TN; ++t)
+#pragma unroll
+            for (int s = 0; s < TM; ++s)
+                acc[t][s] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fp[buf][t], fq[buf][s], acc[t][s], 0, 0, 0);
+    };
+    auto round16 = [&]() {
+        // fp16 accumulation: the running sum is rounded to fp16 at the end of
+        // every aligned 32-deep group of k.
+        if constexpr (ACC16) {
 #pragma unroll
             for (int t = 0; t < TN; ++t)
 #pragma unroll
                 for (int s = 0; s < TM; ++s)
-                    acc[t][s] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fp[t], fq[s], acc[t][s], 0, 0, 0);
-            if constexpr (ACC16) {
-                if (ks & 1) {
-                    // fp16 accumulation: round the running sum to fp16 at the
-                    // end of every aligned 32-deep group of k.
 #pragma unroll
-                    for (int t = 0; t < TN; ++t)
-#pragma unroll
-                        for (int s = 0; s < TM; ++s)
-#pragma unroll
-                            for (int e = 0; e < 16; ++e) acc[t][s][e] = (float)(_Float16)acc[t][s][e];
-                }
-            }
+                    for (int e = 0; e < 16; ++e) acc[t][s][e] = (float)(_Float16)acc[t][s][e];
         }
-        if (more) {
-            sa.store(nxt);
-            sb.store(nxt + BM * ROWB);
-        }
+    };
+
+    // Instruction interleaving hints for the scheduler: each MFMA is paired
+    // with the fragment read (DS read), staging write (DS write) or global
+    // load (VMEM read) that has to overlap it.
+    constexpr int NM = TN * TM;           // MFMAs per 16-deep slice
+    constexpr int NR = TM + TN;           // fragment reads per slice
+    constexpr int NW = CopyA::NWRITE + CopyB::NWRITE;
+    constexpr int NL = CopyA::NLOAD + CopyB::NLOAD;
+
+    // Prologue: step 0 into LDS stage 0 and step 1 under way (into stage 1
+    // or the staging registers), then the first fragments of step 0.
+    if (nk > 0) {
+        copy_step(0, lds);
+        ca.write(lds);
+        cb.write(lds + BM * ROWB);
+        copy_step(1, lds + STAGE);
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
+        read_frags(0, lds, 0);
+    }
+
+    // One reduction step.  On entry LDS stage `cur` holds step kt, step kt+1
+    // is under way (into `nxt` or the staging registers) and fq/fp[0] hold
+    // slice 0 of step kt.
+    for (int kt = 0; kt < nk; ++kt) {
+        char *cur = lds + (kt & 1) * STAGE;
+        char *nxt = lds + ((kt + 1) & 1) * STAGE;
+        // slice 0 (fragments of slice 1 in flight)
+        read_frags(1, cur, 1);
+        mfmas(0);
+        sched_slice<NM, NR, 0, 0>();
+        // slice 1
+        read_frags(0, cur, 2);
+        mfmas(1);
+        round16();
+        sched_slice<NM, NR, 0, 0>();
+        // slice 2, plus the register-staged writes of step kt+1
+        read_frags(1, cur, 3);
+        mfmas(0);
+        ca.write(nxt);
+        cb.write(nxt + BM * ROWB);
+        sched_slice<NM, NR, 0x200, NW>();
+        // Step kt+1 complete in LDS for every wave; every read of `cur` done.
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        // slice 3, plus the first fragments of step kt+1 and the copies of
+        // step kt+2 (into `cur`, now free)
+        read_frags(0, nxt, 0);
+        mfmas(1);
+        round16();
+        copy_step(kt + 2, cur);
+        sched_slice<NM, NR, 0x020, NL>();
     }
 
     // Epilogue on registers: + bias, ReLU, fp16, two 16-byte stores per lane
-    // per 32x32 block.
+    // per 32x32 block (each guarded so an output shared with a neighbouring
+    // tile is stored by its owner only).
 #pragma unroll
     for (int t = 0; t < TN; ++t) {
-        const int j = n0 + wn * WTN + 32 * t + 16 * hi;
+        const int j = nc + wn * WTN + 32 * t + 16 * hi;
         float b[16];
-#pragma unroll
-        for (int e = 0; e < 16; ++e) b[e] = 0.f;
-        if (p.bias != nullptr && j < p.N) {
-            h8 b0 = *reinterpret_cast<const h8 *>(p.bias + j);
-            h8 b1 = j + 8 < p.N ? *reinterpret_cast<const h8 *>(p.bias + j + 8) : zero_h8();
+        if (p.bias != nullptr) {
+            const h8 b0 = *reinterpret_cast<const h8 *>(p.bias + j);
+            const h8 b1 = *reinterpret_cast<const h8 *>(p.bias + j + 8);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 b[e] = (float)b0[e];
                 b[8 + e] = (float)b1[e];
             }
+        } else {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) b[e] = 0.f;
         }
 #pragma unroll
         for (int s = 0; s < TM; ++s) {
-            const int i = m0 + wm * WTM + 32 * s + l32;
+            const int i = mc + wm * WTM + 32 * s + l32;
             h8 o0, o1;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
@@ -315,10 +471,10 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_fast(GemmArgs p)
                 o0[e] = (_Float16)x0;
                 o1[e] = (_Float16)x1;
             }
-            if (i < p.M && j < p.N) {
+            if (i >= m0) {
                 _Float16 *dst = p.C + (int64_t)i * p.ldc + j;
-                *reinterpret_cast<h8 *>(dst) = o0;
-                if (j + 8 < p.N) *reinterpret_cast<h8 *>(dst + 8) = o1;
+                if (j >= n0) *reinterpret_cast<h8 *>(dst) = o0;
+                if (j + 8 >= n0) *reinterpret_cast<h8 *>(dst + 8) = o1;
             }
         }
     }

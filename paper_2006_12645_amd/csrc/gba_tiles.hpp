@@ -57,7 +57,7 @@ template <int BM, int BN, int WM, int WN, int LA, int LB, bool ACC16>
 hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
 {
     dim3 grid((unsigned)(a.tiles_m * a.tiles_n)), block(64 * WM * WN);
-    hipLaunchKernelGGL((gemm_bias_act_fast<BM, BN, WM, WN, LA, LB, ACC16>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((gemm_bias_act_fast<BM, BN, WM, WN, LA, LB, ACC16, true>), grid, block, 0, s, a);
     return hipGetLastError();
 }
 

@@ -109,7 +109,13 @@ def test_tile_table():
                                    (1, 1, 1), (0, 5, 5)])
 def test_select_tile(shape):
     t = gba.select_tile(*shape)
-    assert 0 <= t < gba.num_tiles()
+    M, N, _ = shape
+    if M < 32 or N < 32:
+        assert t == -1
+    else:
+        assert 0 <= t < gba.num_tiles()
+        info = gba.tile_info(t)
+        assert info["bm"] <= M and info["bn"] <= N
 
 
 def test_select_tile_rejects_bad_input():
