@@ -39,16 +39,20 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 bool tile_fits(int tile, int64_t M, int64_t N) { return M >= TILES[tile].bm && N >= TILES[tile].bn; }
 
-// Tile choice by problem shape: the largest block tile that fits inside the
-// problem and still yields enough workgroups to occupy the 256 compute
-// units; failing that, the one with the most workgroups.
-int select_tile(int64_t M, int64_t N, int64_t K)
+// Tile choice by problem shape.  With enough output tiles, the largest block
+// tile that fits inside the problem and still yields a workgroup for each
+// of the 256 compute units.  With few output tiles and a long reduction,
+// intra-workgroup split-K over a small tile (fp32 accumulation only): its
+// four k-groups and four-stage copies keep the memory system busy where
+// the plain tiles would leave most compute units idle.  Otherwise the tile
+// with the most workgroups.
+int select_tile(int64_t M, int64_t N, int64_t K, int accum)
 {
-    (void)K;
     const int64_t CUS = 256;
     static const int order[] = {1, 2, 3, 4, 5, 7, 6, 8, 9};
     for (int t : order)
         if (tile_fits(t, M, N) && ceil_div(M, TILES[t].bm) * ceil_div(N, TILES[t].bn) >= CUS) return t;
+    if (accum == GBA_ACC_F32 && K >= 4096 && tile_fits(13, M, N)) return 13;
     for (int t : {6, 8, 9})
         if (tile_fits(t, M, N)) return t;
     return -1;  // smaller than the smallest tile: general path
@@ -86,7 +90,9 @@ gba_status run_gemm(int la, int lb, int64_t M, int64_t N, int64_t K, const void 
 
     // A requested tile that is larger than the problem is replaced by the
     // library's choice; problems smaller than every tile take the general path.
-    int tile = tile_id >= 0 && tile_fits(tile_id, M, N) ? tile_id : select_tile(M, N, K);
+    const bool tile_ok = tile_id >= 0 && tile_fits(tile_id, M, N) &&
+                         !(accum == GBA_ACC_F16 && TILES[tile_id].sk > 1);
+    int tile = tile_ok ? tile_id : select_tile(M, N, K, accum);
     const bool fast = tile >= 0 && fast_path_ok(la, lb, M, N, K, A, lda, B, ldb, bias, C, ldc);
     if (!fast) tile = -1;
     const TileCfg cfg = fast ? TILES[tile] : GENERIC_TILE;
@@ -214,8 +220,8 @@ extern "C" gba_status gba_tile_info(int tile_id, int *bm, int *bn, int *bk, int 
     if (bm) *bm = c.bm;
     if (bn) *bn = c.bn;
     if (bk) *bk = 64;
-    if (waves) *waves = c.wm * c.wn;
-    if (split_k) *split_k = 1;
+    if (waves) *waves = c.wm * c.wn * c.sk;
+    if (split_k) *split_k = c.sk;
     return GBA_OK;
 }
 
@@ -225,7 +231,7 @@ extern "C" int gba_select_tile(gba_layout layoutA, gba_layout layoutB, int64_t M
     if (!is_layout(layoutA) || !is_layout(layoutB)) return -1;
     if (accum != GBA_ACC_F32 && accum != GBA_ACC_F16) return -1;
     if (M < 0 || N < 0 || K < 0 || M > INT_MAX || N > INT_MAX || K > INT_MAX) return -1;
-    return select_tile(M, N, K);  // -1 also when the general path would run
+    return select_tile(M, N, K, accum);  // -1 also when the general path would run
 }
 
 extern "C" gba_status gba_bias_add_f16(int64_t M, int64_t N, void *C, int64_t ldc, const void *bias,

@@ -5,8 +5,8 @@
 
 namespace gba {
 
-#define GBA_FAST_ENTRY(id, BM, BN, WM, WN) \
-    {&launch_fast<BM, BN, WM, WN, COL, COL, false>, &launch_fast<BM, BN, WM, WN, COL, COL, true>},
+#define GBA_FAST_ENTRY(id, BM, BN, WM, WN, SK, NSTG) \
+    {&launch_fast<BM, BN, WM, WN, SK, NSTG, COL, COL, false>, fast_acc16<BM, BN, WM, WN, SK, NSTG, COL, COL>()},
 
 const LayoutTable &table_CC()
 {

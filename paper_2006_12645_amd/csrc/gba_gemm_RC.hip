@@ -5,8 +5,8 @@
 
 namespace gba {
 
-#define GBA_FAST_ENTRY(id, BM, BN, WM, WN) \
-    {&launch_fast<BM, BN, WM, WN, ROW, COL, false>, &launch_fast<BM, BN, WM, WN, ROW, COL, true>},
+#define GBA_FAST_ENTRY(id, BM, BN, WM, WN, SK, NSTG) \
+    {&launch_fast<BM, BN, WM, WN, SK, NSTG, ROW, COL, false>, fast_acc16<BM, BN, WM, WN, SK, NSTG, ROW, COL>()},
 
 const LayoutTable &table_RC()
 {

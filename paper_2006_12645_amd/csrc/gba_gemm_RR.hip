@@ -5,8 +5,8 @@
 
 namespace gba {
 
-#define GBA_FAST_ENTRY(id, BM, BN, WM, WN) \
-    {&launch_fast<BM, BN, WM, WN, ROW, ROW, false>, &launch_fast<BM, BN, WM, WN, ROW, ROW, true>},
+#define GBA_FAST_ENTRY(id, BM, BN, WM, WN, SK, NSTG) \
+    {&launch_fast<BM, BN, WM, WN, SK, NSTG, ROW, ROW, false>, fast_acc16<BM, BN, WM, WN, SK, NSTG, ROW, ROW>()},
 
 const LayoutTable &table_RR()
 {

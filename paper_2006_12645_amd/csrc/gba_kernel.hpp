@@ -187,6 +187,15 @@ struct FastStage {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+// s_waitcnt vmcnt(VM) lgkmcnt(0): all but the VM most recent global loads
+// done, and every LDS access of this wave done.
+template <int VM>
+__device__ __forceinline__ void wait_vm_lgkm0()
+{
+    static_assert(VM >= 0 && VM < 64, "vmcnt field is 6 bits");
+    __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4));
+}
+
 // 16 bytes per lane from buffer `rs` straight into LDS at `lds` + 16 * lane.
 __device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t rs, char *lds, int voff, int soff)
 {
@@ -273,23 +282,44 @@ struct DmaCopy {
     __device__ __forceinline__ void write(char *) const {}
 };
 
-template <int BM, int BN, int WM, int WN, int LA, int LB, bool ACC16, bool DMA>
-__global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_fast(GemmArgs p)
+// SK > 1: intra-workgroup split-K (Split-K subsection): the workgroup holds
+// SK groups of WM x WN waves; in every step group g multiplies its own
+// 64-deep slab of the reduction (SK slabs per step, each in its own LDS
+// sub-stage), and after the last step the SK partial tiles are summed
+// through LDS before the epilogue.
+// NSTG (a power of two) LDS stages are used when both operands are copied
+// directly into LDS: the copies of a step are then issued NSTG - 1 steps
+// before the step is multiplied, so small tiles that cannot cover the
+// memory latency with work hide it with depth.  Register-staged operands
+// keep two stages.
+template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool DMA>
+__global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs p)
 {
-    constexpr int NT = 64 * WM * WN;
+    constexpr int NTG = 64 * WM * WN;         // threads per k-group
+    constexpr int NT = NTG * SK;
     constexpr int BK = 64;
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int TM = WTM / 32, TN = WTN / 32;
     constexpr int ROWB = BK * 2;              // bytes per LDS row
-    constexpr int STAGE = (BM + BN) * ROWB;   // bytes per LDS stage
+    constexpr int SUB = (BM + BN) * ROWB;     // bytes per k-group sub-stage
+    constexpr int STAGE = SK * SUB;           // bytes per LDS stage
+    constexpr bool DEEP = DMA && LA == ROW && LB == COL;
+    constexpr int NS = DEEP ? NSTG : 2;       // LDS stages
+    static_assert((NS & (NS - 1)) == 0, "stage count must be a power of two");
+    constexpr int PADN = BN + 4;              // fp32 row pitch of the split-K partial tiles
+    constexpr int RED = SK > 1 ? SK * BM * PADN * 4 : 0;
+    constexpr int LDS_BYTES = NS * STAGE > RED ? NS * STAGE : RED;
     static_assert(WTM % 32 == 0 && WTN % 32 == 0, "warp tile must be a multiple of 32x32");
+    static_assert(!(ACC16 && SK > 1), "fp16 accumulation is defined for a single running sum");
 
-    __shared__ __attribute__((aligned(16))) char lds[2 * STAGE];
+    __shared__ __attribute__((aligned(16))) char lds[LDS_BYTES];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wm = wave % WM, wn = wave / WM;
+    const int grp = wave / (WM * WN);         // k-group
+    const int gtid = tid - grp * NTG;         // thread index inside the k-group
+    const int wm = (wave % (WM * WN)) % WM, wn = (wave % (WM * WN)) / WM;
     const int l32 = lane & 31, hi = lane >> 5;
 
     int tm, tn;
@@ -302,12 +332,12 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_fast(GemmArgs p)
     const int mc = m0 + BM <= p.M ? m0 : p.M - BM;
     const int nc = n0 + BN <= p.N ? n0 : p.N - BN;
 
-    using CopyA = std::conditional_t<DMA && LA == ROW, DmaCopy<BM, NT>, RegCopy<BM, NT, LA == ROW>>;
-    using CopyB = std::conditional_t<DMA && LB == COL, DmaCopy<BN, NT>, RegCopy<BN, NT, LB == COL>>;
+    using CopyA = std::conditional_t<DMA && LA == ROW, DmaCopy<BM, NTG>, RegCopy<BM, NTG, LA == ROW>>;
+    using CopyB = std::conditional_t<DMA && LB == COL, DmaCopy<BN, NTG>, RegCopy<BN, NTG, LB == COL>>;
     CopyA ca;
     CopyB cb;
-    ca.init(p.lda, tid);
-    cb.init(p.ldb, tid);
+    ca.init(p.lda, gtid);
+    cb.init(p.ldb, gtid);
 
     // Resource of the step starting at reduction index k0 for each operand.
     auto rsrc_a = [&](int k0) {
@@ -318,14 +348,15 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_fast(GemmArgs p)
         if constexpr (LB == COL) return make_rsrc(p.B + (int64_t)nc * p.ldb + k0, MAX_RECORDS);
         else return make_rsrc(p.B + (int64_t)k0 * p.ldb + nc, MAX_RECORDS);
     };
-    const int nk = (p.K + BK - 1) / BK;
+    const int nk = (p.K + SK * BK - 1) / (SK * BK);
 
-    // Copies of step s: direct-to-LDS operands into `stage`, the others into
-    // their staging registers.  Steps past the last one re-fetch the last
-    // step (into a stage nobody reads again), so every step of the loop
-    // below has the same shape.
+    // Copies of step s (this k-group's slab): direct-to-LDS operands into
+    // `stage`, the others into their staging registers.  Steps past the
+    // last one re-fetch the last step (into a stage nobody reads again), so
+    // every step of the loop below has the same shape.  A slab starting at
+    // or beyond K reads as zeros.
     auto copy_step = [&](int s, char *stage) {
-        const int k0 = (s < nk ? s : nk - 1) * BK;
+        const int k0 = ((s < nk ? s : nk - 1) * SK + grp) * BK;
         const int kleft = p.K - k0;
         const auto ra = rsrc_a(k0);
         const auto rb = rsrc_b(k0);
@@ -394,22 +425,27 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_fast(GemmArgs p)
 
     // Prologue: step 0 into LDS stage 0 and step 1 under way (into stage 1
     // or the staging registers), then the first fragments of step 0.
+    char *const mine = lds + grp * SUB;   // this k-group's sub-stage of stage 0
     if (nk > 0) {
-        copy_step(0, lds);
-        ca.write(lds);
-        cb.write(lds + BM * ROWB);
-        copy_step(1, lds + STAGE);
+        copy_step(0, mine);
+        ca.write(mine);
+        cb.write(mine + BM * ROWB);
+#pragma unroll
+        for (int s = 1; s < NS; ++s) copy_step(s, mine + s * STAGE);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
-        read_frags(0, lds, 0);
+        read_frags(0, mine, 0);
     }
+    // Global loads still allowed in flight at the barrier of step kt: the
+    // copies of steps kt+2 .. kt+NS-1; step kt+1 must have landed.
+    constexpr int VM_AT_BARRIER = (NS - 2) * NL;
 
     // One reduction step.  On entry LDS stage `cur` holds step kt, step kt+1
     // is under way (into `nxt` or the staging registers) and fq/fp[0] hold
     // slice 0 of step kt.
     for (int kt = 0; kt < nk; ++kt) {
-        char *cur = lds + (kt & 1) * STAGE;
-        char *nxt = lds + ((kt + 1) & 1) * STAGE;
+        char *cur = mine + (kt & (NS - 1)) * STAGE;
+        char *nxt = mine + ((kt + 1) & (NS - 1)) * STAGE;
         // slice 0 (fragments of slice 1 in flight)
         read_frags(1, cur, 1);
         mfmas(0);
@@ -426,15 +462,79 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_fast(GemmArgs p)
         cb.write(nxt + BM * ROWB);
         sched_slice<NM, NR, 0x200, NW>();
         // Step kt+1 complete in LDS for every wave; every read of `cur` done.
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
+        if constexpr (VM_AT_BARRIER == 0) {
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+        } else {
+            __builtin_amdgcn_sched_barrier(0);
+            wait_vm_lgkm0<VM_AT_BARRIER>();
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+        }
         // slice 3, plus the first fragments of step kt+1 and the copies of
-        // step kt+2 (into `cur`, now free)
+        // step kt+NS (into `cur`, now free)
         read_frags(0, nxt, 0);
         mfmas(1);
         round16();
-        copy_step(kt + 2, cur);
+        copy_step(kt + NS, cur);
         sched_slice<NM, NR, 0x020, NL>();
+    }
+
+    // Drain the trailing (unused) copies: nothing may still be writing LDS
+    // when it is reused below or released.
+    __builtin_amdgcn_s_waitcnt(0);
+
+    if constexpr (SK > 1) {
+        // Split-K: every k-group writes its partial tile to LDS (fp32, rows
+        // padded by 4 floats so the 32 rows a store touches hit distinct
+        // banks), then all threads sum the SK partials in group order, apply
+        // the epilogue and store 8 contiguous outputs each.
+        __syncthreads();
+        float *part = reinterpret_cast<float *>(lds);
+#pragma unroll
+        for (int t = 0; t < TN; ++t)
+#pragma unroll
+            for (int s = 0; s < TM; ++s) {
+                const int i = wm * WTM + 32 * s + l32;
+                const int j = wn * WTN + 32 * t + 16 * hi;
+                f4 *dst = reinterpret_cast<f4 *>(part + (grp * BM + i) * PADN + j);
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    dst[q] = f4{acc[t][s][4 * q], acc[t][s][4 * q + 1], acc[t][s][4 * q + 2], acc[t][s][4 * q + 3]};
+            }
+        __syncthreads();
+        constexpr int CPR = BN / 8;   // 8-column chunks per row
+        for (int c = tid; c < BM * CPR; c += NT) {
+            const int i = c / CPR, j = (c % CPR) * 8;
+            float x[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[e] = 0.f;
+#pragma unroll
+            for (int g = 0; g < SK; ++g) {
+                const f4 *src = reinterpret_cast<const f4 *>(part + (g * BM + i) * PADN + j);
+                const f4 a0 = src[0], a1 = src[1];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    x[e] += a0[e];
+                    x[4 + e] += a1[e];
+                }
+            }
+            if (p.bias != nullptr) {
+                const h8 bv = *reinterpret_cast<const h8 *>(p.bias + nc + j);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[e] += (float)bv[e];
+            }
+            h8 o;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                float v = x[e];
+                if (p.relu) v = v > 0.f ? v : 0.f;
+                o[e] = (_Float16)v;
+            }
+            if (mc + i >= m0 && nc + j >= n0)
+                *reinterpret_cast<h8 *>(p.C + (int64_t)(mc + i) * p.ldc + nc + j) = o;
+        }
+        return;
     }
 
     // Epilogue on registers: + bias, ReLU, fp16, two 16-byte stores per lane

@@ -17,48 +17,65 @@
 namespace gba {
 
 struct TileCfg {
-    int bm, bn, wm, wn;
+    int bm, bn, wm, wn, sk, nstg;
 };
 
-// X(id, BM, BN, WM, WN): BM output rows x BN output columns per workgroup,
-// WM x WN waves, each owning a (BM/WM) x (BN/WN) warp tile (multiples of
-// 32 x 32, the MFMA block).
-#define GBA_TILE_LIST(X)   \
-    X(0, 256, 256, 2, 2)   \
-    X(1, 256, 256, 2, 4)   \
-    X(2, 256, 128, 2, 2)   \
-    X(3, 128, 256, 2, 2)   \
-    X(4, 128, 128, 2, 2)   \
-    X(5, 128, 64, 2, 2)    \
-    X(6, 64, 64, 2, 2)     \
-    X(7, 64, 128, 2, 2)    \
-    X(8, 32, 64, 1, 2)     \
-    X(9, 32, 32, 1, 1)
+// X(id, BM, BN, WM, WN, SK, NSTG): BM output rows x BN output columns per
+// workgroup, WM x WN waves, each owning a (BM/WM) x (BN/WN) warp tile
+// (multiples of 32 x 32, the MFMA block), times SK k-groups of waves that
+// split each reduction step (intra-workgroup split-K; fp32 accumulation
+// only); NSTG LDS stages when both operands are copied directly into LDS.
+#define GBA_TILE_LIST(X)         \
+    X(0, 256, 256, 2, 2, 1, 2)   \
+    X(1, 256, 256, 2, 4, 1, 2)   \
+    X(2, 256, 128, 2, 2, 1, 2)   \
+    X(3, 128, 256, 2, 2, 1, 2)   \
+    X(4, 128, 128, 2, 2, 1, 2)   \
+    X(5, 128, 64, 2, 2, 1, 2)    \
+    X(6, 64, 64, 2, 2, 1, 2)     \
+    X(7, 64, 128, 2, 2, 1, 2)    \
+    X(8, 32, 64, 1, 2, 1, 2)     \
+    X(9, 32, 32, 1, 1, 1, 2)     \
+    X(10, 64, 64, 1, 1, 4, 2)    \
+    X(11, 64, 64, 2, 2, 2, 4)    \
+    X(12, 32, 64, 1, 1, 4, 2)    \
+    X(13, 32, 32, 1, 1, 4, 4)    \
+    X(14, 128, 128, 2, 2, 2, 2)  \
+    X(15, 64, 128, 1, 2, 2, 2)
 
-constexpr int NUM_TILES = 10;
+constexpr int NUM_TILES = 16;
 
-#define GBA_TILE_CFG(id, BM, BN, WM, WN) TileCfg{BM, BN, WM, WN},
+#define GBA_TILE_CFG(id, BM, BN, WM, WN, SK, NSTG) TileCfg{BM, BN, WM, WN, SK, NSTG},
 constexpr TileCfg TILES[NUM_TILES] = {GBA_TILE_LIST(GBA_TILE_CFG)};
 #undef GBA_TILE_CFG
 
 // Block tile of the general path (any size, leading dimension, alignment).
-constexpr TileCfg GENERIC_TILE = {64, 64, 2, 2};
+constexpr TileCfg GENERIC_TILE = {64, 64, 2, 2, 1, 2};
 
 typedef hipError_t (*LaunchFn)(const GemmArgs &, hipStream_t);
 
-// Per operand-layout pair: fast[tile][acc16] for the aligned fast path,
-// generic[acc16] otherwise.
+// Per operand-layout pair: fast[tile][acc16] for the aligned fast path
+// (null for fp16 accumulation with split-K), generic[acc16] otherwise.
 struct LayoutTable {
     LaunchFn fast[NUM_TILES][2];
     LaunchFn generic[2];
 };
 
-template <int BM, int BN, int WM, int WN, int LA, int LB, bool ACC16>
+template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16>
 hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
 {
-    dim3 grid((unsigned)(a.tiles_m * a.tiles_n)), block(64 * WM * WN);
-    hipLaunchKernelGGL((gemm_bias_act_fast<BM, BN, WM, WN, LA, LB, ACC16, true>), grid, block, 0, s, a);
+    dim3 grid((unsigned)(a.tiles_m * a.tiles_n)), block(64 * WM * WN * SK);
+    hipLaunchKernelGGL((gemm_bias_act_fast<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, true>), grid, block,
+                       0, s, a);
     return hipGetLastError();
+}
+
+// Launch-table entry for fp16 accumulation: none with split-K.
+template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB>
+constexpr LaunchFn fast_acc16()
+{
+    if constexpr (SK == 1) return &launch_fast<BM, BN, WM, WN, SK, NSTG, LA, LB, true>;
+    else return nullptr;
 }
 
 template <int LA, int LB, bool ACC16>

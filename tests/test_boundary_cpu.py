@@ -60,7 +60,7 @@ def gemm(M=64, N=64, K=64, la=0, lb=1, A=FAKE, lda=None, B=FAKE, ldb=None, bias=
     (dict(A=None), gba.GBA_EINVAL),
     (dict(B=None), gba.GBA_EINVAL),
     (dict(C=None), gba.GBA_EINVAL),
-    (dict(tile=10), gba.GBA_EINVAL),
+    (dict(tile=16), gba.GBA_EINVAL),
     (dict(tile=1000), gba.GBA_EINVAL),
     (dict(A=FAKE + 1), gba.GBA_EUNSUPPORTED),
     (dict(C=FAKE + 1), gba.GBA_EUNSUPPORTED),
@@ -96,9 +96,9 @@ def test_tile_table():
     for t in range(n):
         info = gba.tile_info(t)
         assert info["bm"] % 16 == 0 and info["bn"] % 32 == 0 and info["bk"] % 32 == 0
-        assert 1 <= info["waves"] <= 16 and info["split_k"] >= 1
-        # two LDS stages of (bm + bn) x bk fp16 fit in a gfx950 CU's 160 KB
-        assert 2 * (info["bm"] + info["bn"]) * info["bk"] * 2 <= 160 * 1024
+        assert 1 <= info["waves"] <= 16 and info["split_k"] in (1, 2, 4)
+        # two LDS stages of split_k x (bm + bn) x bk fp16 fit in a gfx950 CU's 160 KB
+        assert 2 * info["split_k"] * (info["bm"] + info["bn"]) * info["bk"] * 2 <= 160 * 1024
     with pytest.raises(gba.GbaError):
         gba.tile_info(n)
 
@@ -116,6 +116,16 @@ def test_select_tile(shape):
         assert 0 <= t < gba.num_tiles()
         info = gba.tile_info(t)
         assert info["bm"] <= M and info["bn"] <= N
+
+
+def test_select_tile_split_k_policy():
+    # long reduction, few output tiles: split-K with fp32 accumulation only
+    t = gba.select_tile(64, 512, 32768)
+    assert gba.tile_info(t)["split_k"] > 1
+    t16 = gba.select_tile(64, 512, 32768, accum="f16")
+    assert gba.tile_info(t16)["split_k"] == 1
+    # enough output tiles: no split-K
+    assert gba.tile_info(gba.select_tile(4096, 4096, 8192))["split_k"] == 1
 
 
 def test_select_tile_rejects_bad_input():

@@ -17,7 +17,8 @@ torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
 LAYOUTS = ["RR", "RC", "CR", "CC"]
-NUM_TILES = 10
+NUM_TILES = 16
+SPLITK_TILES = [10, 11, 12, 13, 14, 15]
 
 
 def announce(*what):
@@ -176,6 +177,28 @@ def test_every_tile_config(tile, layout):
     U.assert_close(got, U.oracle_for(A, B, bias), what=f"tile {tile} {layout}")
 
 
+@pytest.mark.parametrize("tile", [11, 13])
+@pytest.mark.parametrize("K", [64, 200, 1000, 5000])
+def test_deep_pipeline_short_and_long_k(tile, K):
+    """Four-stage pipelines with fewer reduction steps than stages (the
+    trailing copies re-fetch the last step) and with many steps."""
+    M, N = 136, 200
+    announce("deep", tile, K)
+    A, B, bias = D.random_problem(3000 + tile + K, M, N, K)
+    got = run_gpu(A, B, bias, "RC", tile=tile).cpu().numpy()
+    U.assert_close(got, U.oracle_for(A, B, bias), what=f"deep tile {tile} K={K}")
+
+
+def test_long_k_selects_split_k():
+    """A long reduction over few output tiles takes the split-K tile."""
+    M, N, K = 96, 320, 8192
+    announce("long-K selection")
+    assert gba.tile_info(gba.select_tile(M, N, K))["split_k"] > 1
+    A, B, bias = D.random_problem(3100, M, N, K)
+    got = run_gpu(A, B, bias, "RC").cpu().numpy()
+    U.assert_close(got, U.oracle_for(A, B, bias), what="long-K")
+
+
 @pytest.mark.parametrize("tile", range(NUM_TILES))
 def test_every_tile_config_f16acc(tile):
     M, N, K = 136, 248, 520
@@ -183,6 +206,30 @@ def test_every_tile_config_f16acc(tile):
     A, B, bias = D.random_problem(1100 + tile, M, N, K)
     got = run_gpu(A, B, bias, "RC", accum="f16", tile=tile).cpu().numpy()
     U.assert_close(got, U.oracle_for(A, B, bias), accum="f16", what=f"tile {tile} f16")
+
+
+@pytest.mark.parametrize("tile", SPLITK_TILES)
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("K", [64, 104, 136, 1000])
+def test_split_k_partial_slabs(tile, layout, K):
+    """Intra-workgroup split-K with reduction lengths that leave some k-groups
+    a partial slab or none at all in the last step."""
+    M, N = 136, 200
+    announce("split-K", tile, layout, K)
+    A, B, bias = D.random_problem(2000 + tile * 7 + K, M, N, K)
+    got = run_gpu(A, B, bias, layout, tile=tile).cpu().numpy()
+    U.assert_close(got, U.oracle_for(A, B, bias), what=f"split-K tile {tile} {layout} K={K}")
+
+
+def test_split_k_integer_bit_exact():
+    """Split-K sums partials in a different order; on integer data the result
+    is still exact."""
+    M, N, K = 192, 256, 2040
+    announce("split-K integer exact")
+    A, B, bias = D.random_problem(78, M, N, K, dist="int")
+    for tile in SPLITK_TILES:
+        got = run_gpu(A, B, bias, "RC", tile=tile).cpu().numpy().astype(np.float64)
+        assert np.array_equal(got, U.oracle_for(A, B, bias)), tile
 
 
 RAGGED = [1, 7, 31, 33, 127, 129]
