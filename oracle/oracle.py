@@ -6,7 +6,8 @@ benchmark's CPU-baseline leg, never by the HIP library or its binding.
 Arrays are numpy: fp16 operands are passed as their raw bit patterns, the
 result comes back as float64.  See oracle_gba.c for the definition computed
 (the Problem Statement section's matmul followed by the ReLU-of-add
-statement, evaluated in binary64 with k ascending).
+statement, and the prologue / sum-of-matmuls / other-pointwise-op idioms,
+evaluated in binary64 with k ascending).
 """
 import ctypes
 import os
@@ -16,7 +17,8 @@ import numpy as np
 from . import build_oracle
 
 ROW, COL = 0, 1
-ACT_NONE, ACT_RELU = 0, 1
+ACT_NONE, ACT_RELU, ACT_SIGMOID, ACT_TANH = 0, 1, 2, 3
+BIAS_NONE, BIAS_ROW, BIAS_FULL = 0, 1, 2
 
 _lib = None
 
@@ -31,6 +33,13 @@ def load_library(path):
     lib.oracle_gemm_bias_act_rows_f64.argtypes = [
         ctypes.c_int, ctypes.c_int, i64, i64, i64, vp, i64, vp, i64, vp,
         ctypes.c_int, vp, i64, vp, i64, ctypes.c_int]
+    ci = ctypes.c_int
+    lib.oracle_fused_rows_f64.restype = ci
+    lib.oracle_fused_rows_f64.argtypes = [
+        ci, ci, i64, i64, i64, vp, i64, vp, i64,          # layouts, M N K, A lda, B ldb
+        ci, ci, i64, vp, i64, vp, i64,                    # pro_relu, second, K2, P ldp, Q ldq
+        ci, ci, vp, i64, ci,                              # bias kind/sign, bias ldbias, act
+        vp, i64, vp, i64, ci]                             # rows nrows, out ldo, nthreads
     return lib
 
 
@@ -98,6 +107,49 @@ def gemm_bias_act(a_store, layout_a, b_store, layout_b, M, N, K, bias=None,
         int(layout_a), int(layout_b), int(M), int(N), int(K), _ptr(a), int(lda), _ptr(b), int(ldb),
         _ptr(bi), int(act), _ptr(r), int(nrows), _ptr(out), int(max(N, 1)),
         int(nthreads or default_threads()))
+    if rc != 0:
+        raise ValueError(f"oracle rejected the arguments (rc={rc})")
+    return out
+
+
+def _ld(store, default):
+    return store.shape[1] if store is not None and store.ndim == 2 else default
+
+
+def fused(a_store, layout_a, b_store, layout_b, M, N, K, *, prologue_relu=False,
+          second=0, p_store=None, q_store=None, K2=0, bias=None, bias_kind=None,
+          bias_sign=1, act=ACT_RELU, lda=None, ldb=None, ldp=None, ldq=None, ldbias=None,
+          rows=None, nthreads=None, lib=None):
+    """Oracle of the general fused operation as float64, shape (len(rows) or M, N).
+
+    ``second`` is 0 (one product), +1 (add P.Q) or -1 (subtract P.Q); P and
+    Q are stored like A and B.  ``bias`` is a length-N vector (bias_kind
+    BIAS_ROW, the default for a 1-D bias) or an M x ldbias array (BIAS_FULL,
+    the default for a 2-D bias); ``bias_sign`` -1 subtracts it.
+    """
+    lib = lib or _load()
+    a, b = _as_bits(a_store), _as_bits(b_store)
+    pp, qq = _as_bits(p_store), _as_bits(q_store)
+    bi = _as_bits(bias)
+    if bias_kind is None:
+        bias_kind = BIAS_NONE if bi is None else (BIAS_ROW if bi.ndim == 1 else BIAS_FULL)
+    if ldbias is None:
+        ldbias = bi.shape[1] if bi is not None and bi.ndim == 2 else N
+    lda = lda if lda is not None else _ld(a, K if layout_a == ROW else M)
+    ldb = ldb if ldb is not None else _ld(b, N if layout_b == ROW else K)
+    ldp = ldp if ldp is not None else _ld(pp, K2 if layout_a == ROW else M)
+    ldq = ldq if ldq is not None else _ld(qq, N if layout_b == ROW else K2)
+    if rows is None:
+        r, nrows = None, M
+    else:
+        r = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+        nrows = r.shape[0]
+    out = np.zeros((nrows, N), dtype=np.float64)
+    rc = lib.oracle_fused_rows_f64(
+        int(layout_a), int(layout_b), int(M), int(N), int(K), _ptr(a), int(lda), _ptr(b), int(ldb),
+        int(bool(prologue_relu)), int(second), int(K2), _ptr(pp), int(ldp), _ptr(qq), int(ldq),
+        int(bias_kind), int(bias_sign), _ptr(bi), int(ldbias), int(act),
+        _ptr(r), int(nrows), _ptr(out), int(max(N, 1)), int(nthreads or default_threads()))
     if rc != 0:
         raise ValueError(f"oracle rejected the arguments (rc={rc})")
     return out

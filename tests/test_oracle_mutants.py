@@ -9,6 +9,7 @@ import pytest
 from oracle import build_oracle
 from oracle import oracle as O
 import oracle_pins as P
+import oracle_pins_fused as PF
 
 # (name, text in oracle_gba.c, replacement) -- each a plausible slip.
 MUTANTS = [
@@ -37,6 +38,32 @@ MUTANTS = [
      "const double *brow = J->Bd + (J->K - 1 - k) * J->N;"),
 ]
 
+# Slips in the wider-idiom oracle (prologue, second product, bias kinds and
+# signs, Sigmoid/Tanh); none of them reads outside the operands.
+MUTANTS += [
+    ("prologue_abs", "v = v > 0.0 ? v : 0.0;", "v = v > 0.0 ? v : -v;"),
+    ("prologue_ignored", "if (pro_relu)\n        v = v > 0.0 ? v : 0.0;", "if (0)\n        v = v > 0.0 ? v : 0.0;"),
+    ("prologue_negative_part", "v = v > 0.0 ? v : 0.0;", "v = v < 0.0 ? v : 0.0;"),
+    ("second_sign_flipped", "c[j] - r[j]", "c[j] + r[j]"),
+    ("second_always_added", "J->second > 0 ? c[j] + r[j]", "J->second != 0 ? c[j] + r[j]"),
+    ("second_last_k_dropped", "J->Qd, J->K2, i, r)", "J->Qd, J->K2 - 1, i, r)"),
+    ("second_uses_lda", "product_row(J, J->P, J->ldp,", "product_row(J, J->P, J->lda,"),
+    ("full_bias_ignores_ld", "J->bias[i * J->ldbias + j]", "J->bias[i * J->N + j]"),
+    ("full_bias_row_zero", "J->bias[i * J->ldbias + j]", "J->bias[j]"),
+    ("bias_sign_ignored", "pre = J->bias_sign > 0 ? z + b : z - b;", "pre = z + b;"),
+    ("sigmoid_sign", "1.0 / (1.0 + exp(-x))", "1.0 / (1.0 + exp(x))"),
+    ("sigmoid_scale", "1.0 / (1.0 + exp(-x))", "1.0 / (1.0 + exp(-2.0 * x))"),
+    ("tanh_half_argument", "return tanh(x);", "return tanh(0.5 * x);"),
+    ("tanh_as_sigmoid", "case OR_ACT_TANH: return tanh(x);", "case OR_ACT_TANH: return 1.0 / (1.0 + exp(-x));"),
+    ("fused_relu_leaky", "case OR_ACT_RELU: return x > 0.0 ? x : 0.0;", "case OR_ACT_RELU: return x > 0.0 ? x : 0.01 * x;"),
+    ("fused_first_k_dropped", "for (int64_t k = 0; k < K; ++k) {\n        double x", "for (int64_t k = 1; k < K; ++k) {\n        double x"),
+    ("fused_q_rows_reversed", "d[k * N + j] = oracle_f16_to_f64", "d[(K - 1 - k) * N + j] = oracle_f16_to_f64"),
+    ("fused_a_k_reversed", "left_elem(J->layout_a, X, ldx, i, k, J->pro_relu)",
+     "left_elem(J->layout_a, X, ldx, i, K - 1 - k, J->pro_relu)"),
+]
+
+ALL_PINS = P.PINS + PF.PINS
+
 
 def _build_mutant(tmp_path, name, old, new):
     src = open(build_oracle.SRC).read()
@@ -54,7 +81,7 @@ def _build_mutant(tmp_path, name, old, new):
 def test_mutant_is_caught(tmp_path, name, old, new):
     lib = _build_mutant(tmp_path, name, old, new)
     failed = []
-    for pin in P.PINS:
+    for pin in ALL_PINS:
         try:
             pin(lib)
         except (AssertionError, ValueError):
@@ -64,5 +91,5 @@ def test_mutant_is_caught(tmp_path, name, old, new):
 
 def test_unmutated_copy_passes(tmp_path):
     lib = _build_mutant(tmp_path, "none", "#include <math.h>", "#include <math.h>")
-    for pin in P.PINS:
+    for pin in ALL_PINS:
         pin(lib)
