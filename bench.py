@@ -10,6 +10,11 @@ the unfused three-launch chain (GEMM, bias add, ReLU) and the plain GEMM on
 the same inputs, the roofline position of the fused kernel, and the CPU
 oracle timed on a bounded sample of the same problem.
 
+--workload prologue4096_RC times relu(A).B + bias -> ReLU (against a ReLU
+pass over A followed by the fused GEMM), --workload sum4096_RC times
+A.B + P.Q + bias -> ReLU with K2 = K (against two GEMMs, an add, a bias add
+and a ReLU); their metric counts 2MN(K + K2) flops.
+
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--tile ID]
                     [--report PATH] [--no-cpu]
 """
@@ -72,28 +77,32 @@ def time_launches(fn, steps, warmup, torch):
     return start.elapsed_time(stop) / steps
 
 
-def cpu_baseline(w, A, B, bias, target_s=12.0):
+def cpu_baseline(w, A, B, bias, P=None, Q=None, target_s=12.0):
     """The oracle on a bounded sample of output rows of the same problem."""
-    import numpy as np
     from oracle import oracle as O
     from paper_2006_12645_amd import datagen as D
     a_st, b_st = D.store(A, D.ROW), D.store(B, D.COL)
+    K2 = w.extra.get("K2", 0) if P is not None else 0
+    kw = dict(prologue_relu=w.extra.get("prologue") == "relu", bias=bias, act=O.ACT_RELU)
+    if P is not None:
+        kw.update(second=1, p_store=D.store(P, D.ROW), q_store=D.store(Q, D.COL), K2=K2)
     threads = O.default_threads()
+
+    def run(rows):
+        t0 = time.perf_counter()
+        O.fused(a_st, D.ROW, b_st, D.COL, w.M, w.N, w.K, rows=rows, nthreads=threads, **kw)
+        return time.perf_counter() - t0
+
     rows = list(range(min(w.M, 4 * threads)))
-    t0 = time.perf_counter()
-    O.gemm_bias_act(a_st, D.ROW, b_st, D.COL, w.M, w.N, w.K, bias=bias, rows=rows, nthreads=threads)
-    dt = time.perf_counter() - t0
+    dt = run(rows)
     # grow the sample to about target_s of work
     nrows = int(min(w.M, max(len(rows), len(rows) * target_s / max(dt, 1e-3))))
-    rows = list(range(nrows))
-    t0 = time.perf_counter()
-    O.gemm_bias_act(a_st, D.ROW, b_st, D.COL, w.M, w.N, w.K, bias=bias, rows=rows, nthreads=threads)
-    dt = time.perf_counter() - t0
-    flops = 2.0 * nrows * w.N * w.K
-    del np
+    dt = run(list(range(nrows)))
+    flops = 2.0 * nrows * w.N * (w.K + K2)
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": f"{nrows} of {w.M} output rows (all {w.N} columns, full K={w.K}) of the "
-                      f"same {w.name} problem, fp64, {dt:.1f} s"}
+            "sample": f"{nrows} of {w.M} output rows (all {w.N} columns, full reduction "
+                      f"K={w.K}{f' + K2={K2}' if K2 else ''}) of the same {w.name} problem, "
+                      f"fp64, {dt:.1f} s"}
 
 
 def main():
@@ -141,11 +150,53 @@ def main():
     dB = torch.from_numpy(np.ascontiguousarray(B.T)).cuda().t()        # column-major
     dbias = torch.from_numpy(bias).cuda()
     out = torch.empty((w.M, w.N), dtype=torch.float16, device="cuda")
-    tile = args.tile if args.tile is not None else gba.select_tile(w.M, w.N, w.K)
+    prologue = w.extra.get("prologue")
+    P = Q = None
+    K2 = 0
+    if "second" in w.extra:
+        P, Q = D.second_inputs(w)
+        K2 = w.extra["K2"]
+        dP = torch.from_numpy(P).cuda()
+        dQ = torch.from_numpy(np.ascontiguousarray(Q.T)).cuda().t()
+    tile = args.tile if args.tile is not None else gba.select_tile(w.M, w.N, w.K + K2)
 
-    fused = lambda: gba.gemm_bias_act(dA, dB, dbias, act="relu", out=out, tile=tile)
-    plain = lambda: gba.gemm_bias_act(dA, dB, None, act="none", out=out, tile=tile)
-    unfused = lambda: gba.unfused_gemm_bias_relu(dA, dB, dbias, out=out, tile=tile)
+    if prologue is None and P is None:
+        # the headline: gemm_bias_act, and the paper's unfused three-launch chain
+        fused = lambda: gba.gemm_bias_act(dA, dB, dbias, act="relu", out=out, tile=tile)
+        plain = lambda: gba.gemm_bias_act(dA, dB, None, act="none", out=out, tile=tile)
+        unfused = lambda: gba.unfused_gemm_bias_relu(dA, dB, dbias, out=out, tile=tile)
+        idiom = "GEMM+bias+ReLU"
+        chain = "GEMM, bias add, ReLU"
+        plain_leg = "GEMM only (no bias, no activation)"
+    elif P is None:
+        # relu(A).B + bias -> ReLU; unfused: ReLU pass over A, then the fused GEMM
+        a_relu = dA.clone()
+        fused = lambda: gba.fused_gemm(dA, dB, prologue="relu", bias=dbias, act="relu", out=out,
+                                       tile=tile)
+        plain = lambda: gba.gemm_bias_act(dA, dB, dbias, act="relu", out=out, tile=tile)
+
+        def unfused():
+            gba.relu_(a_relu)
+            gba.gemm_bias_act(a_relu, dB, dbias, act="relu", out=out, tile=tile)
+        idiom = "ReLU-prologue GEMM+bias+ReLU"
+        chain = "ReLU over A, GEMM+bias+ReLU"
+        plain_leg = "GEMM+bias+ReLU without the prologue"
+    else:
+        # A.B + P.Q + bias -> ReLU; unfused: two GEMMs, add, bias add, ReLU
+        tmp = torch.empty_like(out)
+        fused = lambda: gba.fused_gemm(dA, dB, P=dP, Q=dQ, bias=dbias, act="relu", out=out,
+                                       tile=tile)
+        plain = lambda: gba.gemm_bias_act(dA, dB, dbias, act="relu", out=out, tile=tile)
+
+        def unfused():
+            gba.gemm_bias_act(dA, dB, None, act="none", out=out, tile=tile)
+            gba.gemm_bias_act(dP, dQ, None, act="none", out=tmp, tile=tile)
+            gba.add_(out, tmp)
+            gba.bias_add_(out, dbias)
+            gba.relu_(out)
+        idiom = "Add(GEMM,GEMM)+bias+ReLU"
+        chain = "GEMM, GEMM, add, bias add, ReLU"
+        plain_leg = "GEMM+bias+ReLU of A.B alone"
 
     torch.cuda.synchronize()
     ms = time_launches(fused, args.steps, args.warmup, torch)
@@ -160,18 +211,20 @@ def main():
         ms_unfused = time_launches(unfused, args.steps, args.warmup, torch)
         ms_fused2 = time_launches(fused, args.steps, 0, torch)
 
-    flops = 2.0 * w.M * w.N * w.K
+    flops = 2.0 * w.M * w.N * (w.K + K2)
     tflops = flops / (ms * 1e-3) / 1e12
-    algo_bytes = 2.0 * (w.M * w.K + w.K * w.N + w.M * w.N + w.N)
+    algo_bytes = 2.0 * (w.M * w.K + w.K * w.N + w.M * K2 + K2 * w.N + w.M * w.N + w.N)
     info = gba.tile_info(tile)
 
     cpu = None
     if not args.no_cpu:
-        cpu = cpu_baseline(w, A, B, bias)
+        cpu = cpu_baseline(w, A, B, bias, P, Q)
 
     traffic = stored_traffic(w.name)
+    metric = METRIC if w.name == HEADLINE else (
+        f"fused {idiom} TFLOP/s (2MN(K+K2)/t) fp16 on 1 MI355X; % of MFMA peak")
     line = {
-        "metric": METRIC,
+        "metric": metric,
         "value": round(tflops, 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -183,9 +236,11 @@ def main():
         "vs_baseline": None,
         "dtype": "f16",
         "data": "synthetic",
-        "config": {"workload": f"{w.name}: fused fp16 GEMM+bias+ReLU M={w.M} N={w.N} K={w.K}, "
-                               f"A row-major, B column-major, fp32 accumulation",
-                   "M": w.M, "N": w.N, "K": w.K, "layout": "RC", "accum": "f32",
+        "config": {"workload": f"{w.name}: fused fp16 {idiom} M={w.M} N={w.N} K={w.K}"
+                               f"{f' K2={K2}' if K2 else ''}, A row-major, B column-major, "
+                               f"fp32 accumulation",
+                   "M": w.M, "N": w.N, "K": w.K, **({"K2": K2} if K2 else {}),
+                   "layout": "RC", "accum": "f32",
                    "tile": dict(id=tile, **info), "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_F16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(tflops / PEAK_F16_TFLOPS, 4),
@@ -194,9 +249,11 @@ def main():
         "extra": None if args.fused_only else {
             "frac_of_fp16_peak": round(tflops / PEAK_F16_TFLOPS, 4),
             "fused_ms_second_pass": round(ms_fused2, 5),
+            "plain_leg": plain_leg,
             "plain_gemm_ms": round(ms_plain, 5),
-            "plain_gemm_tflops": round(flops / (ms_plain * 1e-3) / 1e12, 2),
-            "unfused_3launch_ms": round(ms_unfused, 5),
+            "plain_gemm_tflops": round(2.0 * w.M * w.N * w.K / (ms_plain * 1e-3) / 1e12, 2),
+            "unfused_chain": chain,
+            "unfused_chain_ms": round(ms_unfused, 5),
             "fused_vs_unfused_speedup": round(ms_unfused / ms, 3),
             "fused_algorithmic_GBps": round(algo_bytes / (ms * 1e-3) / 1e9, 1),
         },

@@ -3,11 +3,14 @@
  *
  * C ABI of libgba.so.  Plain pointers and sizes only; C99 compatible.
  *
- * The operation is the matmul followed by the pointwise ReLU-of-add
- * statement of the paper's Problem Statement section (Listing 1 and its
- * expression tree, whose root is ReLU over the add of the matmul result and
- * the bias), computed in ONE kernel so the matmul result never goes to
- * global memory (Kernel Fusion section, "Pointwise Operations in Epilogue").
+ * The headline operation is the matmul followed by the pointwise
+ * ReLU-of-add statement of the paper's Problem Statement section (Listing 1
+ * and its expression tree, whose root is ReLU over the add of the matmul
+ * result and the bias), computed in ONE kernel so the matmul result never
+ * goes to global memory (Kernel Fusion section, "Pointwise Operations in
+ * Epilogue").  gba_fused_gemm adds the section's other idioms: a ReLU
+ * prologue, a second matmul feeding the epilogue, a full or subtracted bias
+ * and the Sigmoid and Tanh activations.
  * Operands may be row- or column-major, the four layout specialisations of
  * the Matmul Compute Decomposition section.
  *
@@ -35,7 +38,9 @@ extern "C" {
 typedef struct ihipStream_t *gba_stream_t;
 
 typedef enum { GBA_ROW_MAJOR = 0, GBA_COL_MAJOR = 1 } gba_layout;
-typedef enum { GBA_ACT_NONE = 0, GBA_ACT_RELU = 1 } gba_act;
+/* Epilogue activation (the pointwise ops of the Introduction's scope):
+ * identity, ReLU max(x, 0), Sigmoid 1 / (1 + exp(-x)), Tanh. */
+typedef enum { GBA_ACT_NONE = 0, GBA_ACT_RELU = 1, GBA_ACT_SIGMOID = 2, GBA_ACT_TANH = 3 } gba_act;
 typedef enum { GBA_ACC_F32 = 0, GBA_ACC_F16 = 1 } gba_acc;
 typedef enum {
     GBA_OK = 0,
@@ -53,7 +58,9 @@ typedef enum {
  * with products summed in fp32 (accum == GBA_ACC_F32; fp16 inputs and fp32
  * accumulation as in the Background section) or with the running sum rounded
  * to fp16 after every aligned group of 32 k values (accum == GBA_ACC_F16).
- * The bias add and ReLU are done in fp32 and rounded once to fp16 (RNE).
+ * The bias add and activation are done in fp32 and rounded once to fp16
+ * (RNE).  act may also be GBA_ACT_SIGMOID or GBA_ACT_TANH (see
+ * gba_fused_gemm for their accuracy).
  *
  * Layout and leading dimensions (BLAS meaning):
  *     A(i,k) = layoutA == GBA_ROW_MAJOR ? A[i*lda + k] : A[k*lda + i]
@@ -102,6 +109,91 @@ gba_status gemm_bias_act_tile(gba_layout layoutA, gba_layout layoutB,
                               gba_act act, gba_acc accum, int tile_id,
                               gba_stream_t stream);
 
+/* Left-operand prologue (Listing 4, ReLU + Matmul). */
+typedef enum { GBA_PRO_NONE = 0, GBA_PRO_RELU = 1 } gba_prologue;
+/* Second product (Listing 5, Sum of Matmuls): none, A.B + P.Q, A.B - P.Q. */
+typedef enum { GBA_SECOND_NONE = 0, GBA_SECOND_ADD = 1, GBA_SECOND_SUB = 2 } gba_second;
+/* Bias shape: none, fp16[N] broadcast over rows, or a full M x N fp16 tile. */
+typedef enum { GBA_BIAS_NONE = 0, GBA_BIAS_ROW = 1, GBA_BIAS_FULL = 2 } gba_bias_kind;
+/* Add or subtract the bias. */
+typedef enum { GBA_OP_ADD = 0, GBA_OP_SUB = 1 } gba_op;
+
+/*
+ * gba_fused_desc -- one request of gba_fused_gemm.  Fill it with
+ * gba_fused_desc_init first (which selects: row-major A and B, no prologue,
+ * no second product, no bias, no activation, fp32 accumulation, library tile
+ * choice), then set what the request needs.  Every pointer is a DEVICE
+ * pointer; a field that the request does not use is ignored.
+ */
+typedef struct gba_fused_desc {
+    gba_layout layoutA, layoutB;  /* also the layouts of P and Q */
+    int64_t M, N, K;
+    const void *A;                /* A(i,k): ROW A[i*lda+k] (lda >= K), COL A[k*lda+i] (lda >= M) */
+    int64_t lda;
+    const void *B;                /* B(k,j): ROW B[k*ldb+j] (ldb >= N), COL B[j*ldb+k] (ldb >= K) */
+    int64_t ldb;
+    gba_prologue prologue;        /* applied to A and, with a second product, to P */
+    gba_second second;
+    int64_t K2;                   /* reduction length of P.Q */
+    const void *P;                /* M x K2, stored like A with leading dimension ldp */
+    int64_t ldp;
+    const void *Q;                /* K2 x N, stored like B with leading dimension ldq */
+    int64_t ldq;
+    gba_bias_kind bias_kind;
+    gba_op bias_op;
+    const void *bias;             /* ROW: bias[j]; FULL: bias[i*ldbias + j], ldbias >= N */
+    int64_t ldbias;
+    gba_act act;
+    gba_acc accum;
+    void *C;                      /* output, row-major: C[i*ldc + j], ldc >= N */
+    int64_t ldc;
+    int tile_id;                  /* < 0: library's choice; else as gemm_bias_act_tile */
+} gba_fused_desc;
+
+/* Set *desc to the defaults listed above (tile_id = -1).  NULL is ignored. */
+void gba_fused_desc_init(gba_fused_desc *desc);
+
+/*
+ * gba_fused_gemm -- the four computation idioms of the paper's scope
+ * (Introduction) in one kernel: a matmul with a pointwise prologue
+ * (Pointwise Operations in Prologue, Listing 4), with a pointwise epilogue
+ * (Pointwise Operations in Epilogue, Listing 1), and two matmuls of the same
+ * output shape feeding a pointwise op (Matmuls with Pointwise Epilogue,
+ * Listing 5).  For 0<=i<M, 0<=j<N:
+ *
+ *     pro(x)   = prologue == GBA_PRO_RELU ? max(x, 0) : x
+ *     Cp(i,j)  = sum_{k<K}  pro(A(i,k)) * B(k,j)
+ *     R(i,j)   = sum_{k<K2} pro(P(i,k)) * Q(k,j)                 (second != NONE)
+ *     Z(i,j)   = Cp + R (SECOND_ADD), Cp - R (SECOND_SUB), Cp (SECOND_NONE)
+ *     pre(i,j) = Z +/- bias(i,j)   (bias_op; no term for GBA_BIAS_NONE)
+ *     C[i*ldc + j] = fp16(act(pre))
+ *
+ * Neither Cp nor R ever reaches global memory: both products are summed in
+ * ONE fp32 running sum per output (A.B's terms, then P.Q's, negated for
+ * SECOND_SUB), so the P.Q operands may have a different reduction length
+ * K2 as long as the output shape matches.  GBA_ACC_F16 rounds that running
+ * sum to fp16 after every aligned group of 32 k values of each product.
+ * The bias term and activation are evaluated in fp32 and the result rounded
+ * once to fp16 (RNE).  Sigmoid and Tanh use the hardware exp2 and
+ * reciprocal approximations (Tanh from its Taylor series for |x| < 1/16):
+ * within a few fp32 ulps of the result, far below the fp16 rounding.
+ *
+ * Fast path: 16-byte aligned A, B, C and (if used) P, Q, bias; lda, ldb,
+ * ldc (and ldp, ldq, ldbias when used) multiples of 8 and below 2^21 for
+ * the operands; N and the contiguous extents of all operands multiples of 8.
+ * Anything else takes the general kernel.  Outputs must not alias inputs.
+ *
+ * Degenerate sizes: M == 0 or N == 0 -> GBA_OK, nothing launched; K == 0
+ * or K2 == 0 make that product's empty sum zero.
+ * Errors: GBA_EINVAL for desc == NULL, a bad enum, a tile_id at or beyond
+ * gba_num_tiles(), negative sizes or leading dimensions, a leading
+ * dimension below its extent, or a NULL pointer that the request reads
+ * (A/B when K > 0, P/Q when K2 > 0, bias when bias_kind != NONE, C);
+ * GBA_EUNSUPPORTED for M, N, K or K2 above 2^31-1 or pointers not 2-byte
+ * aligned; GBA_EHIP if the launch fails.  Nothing is launched on error.
+ */
+gba_status gba_fused_gemm(const gba_fused_desc *desc, gba_stream_t stream);
+
 /* Number of tile configurations compiled into the library. */
 int gba_num_tiles(void);
 
@@ -130,13 +222,17 @@ int gba_select_tile(gba_layout layoutA, gba_layout layoutB, int64_t M, int64_t N
  * leading dimension ldc >= N and is updated in place:
  *   gba_bias_add_f16: C[i*ldc+j] = fp16(C[i*ldc+j] + bias[j])  (fp32 add)
  *   gba_relu_f16:     C[i*ldc+j] = max(C[i*ldc+j], 0)
- * Errors: GBA_EINVAL for negative sizes, ldc < N, NULL C or bias when the
- * work is non-empty; GBA_EUNSUPPORTED for sizes above 2^31-1 or pointers
- * not 2-byte aligned; GBA_EHIP if the launch fails.
+ *   gba_add_f16:      C[i*ldc+j] = fp16(C[i*ldc+j] + X[i*ldx+j])  (fp32 add;
+ *                     the separate add of two matmul results, Listing 5)
+ * Errors: GBA_EINVAL for negative sizes, ldc < N (or ldx < N), NULL C, bias
+ * or X when the work is non-empty; GBA_EUNSUPPORTED for sizes above 2^31-1
+ * or pointers not 2-byte aligned; GBA_EHIP if the launch fails.
  */
 gba_status gba_bias_add_f16(int64_t M, int64_t N, void *C, int64_t ldc, const void *bias,
                             gba_stream_t stream);
 gba_status gba_relu_f16(int64_t M, int64_t N, void *C, int64_t ldc, gba_stream_t stream);
+gba_status gba_add_f16(int64_t M, int64_t N, void *C, int64_t ldc, const void *X, int64_t ldx,
+                       gba_stream_t stream);
 
 /* Static, human-readable name of a status code. */
 const char *gba_status_string(gba_status status);

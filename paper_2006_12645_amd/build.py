@@ -1,7 +1,9 @@
 """Build libgba.so (gfx950 only) in-tree with hipcc.
 
-Each translation unit under csrc/ is compiled in parallel, then linked into
-``paper_2006_12645_amd/libgba.so``.  Every hipcc line carries
+The entry points (csrc/gba_api.hip) and one kernel-instantiation unit per
+operand-layout pair and kernel variant (csrc/gba_gemm_unit.hip compiled with
+GBA_LA, GBA_LB, GBA_PRO, GBA_DUAL set) are compiled in parallel, then linked
+into ``paper_2006_12645_amd/libgba.so``.  Every hipcc line carries
 ``-Xclang -target-feature -Xclang -packed-fp32-ops`` so the device compiler
 never forms packed fp32 instructions.
 """
@@ -18,8 +20,12 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libgba.so")
 ARCH = "gfx950"
 
-SOURCES = ["gba_api.hip", "gba_gemm_RR.hip", "gba_gemm_RC.hip", "gba_gemm_CR.hip",
-           "gba_gemm_CC.hip"]
+# (source, extra defines, object name)
+UNITS = [("gba_api.hip", [], "gba_api.o")] + [
+    ("gba_gemm_unit.hip",
+     [f"-DGBA_LA={la}", f"-DGBA_LB={lb}", f"-DGBA_PRO={pro}", f"-DGBA_DUAL={dual}"],
+     f"gba_gemm_{'RC'[la]}{'RC'[lb]}_p{pro}d{dual}.o")
+    for la in (0, 1) for lb in (0, 1) for pro in (0, 1) for dual in (0, 1)]
 HIPCC_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall",
                "-Wno-unused-function", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
                "-I", INCLUDE, "-I", CSRC]
@@ -32,9 +38,10 @@ def _hipcc():
     raise RuntimeError("hipcc not found")
 
 
-def _compile(src, verbose):
-    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [_hipcc()] + HIPCC_FLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
+def _compile(unit, verbose):
+    src, defines, name = unit
+    obj = os.path.join(BUILD, name)
+    cmd = [_hipcc()] + HIPCC_FLAGS + defines + ["-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -42,7 +49,7 @@ def _compile(src, verbose):
     noise = "is not a recognized feature for this target"
     err = "\n".join(l for l in r.stderr.splitlines() if noise not in l)
     if r.returncode != 0:
-        raise RuntimeError(f"hipcc failed on {src}:\n{err}")
+        raise RuntimeError(f"hipcc failed on {src} {' '.join(defines)}:\n{err}")
     if err.strip() and verbose:
         print(err, flush=True)
     return obj
@@ -50,9 +57,9 @@ def _compile(src, verbose):
 
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    jobs = max(1, min(len(SOURCES), int(os.environ.get("MAX_JOBS", "8"))))
+    jobs = max(1, min(len(UNITS), int(os.environ.get("MAX_JOBS", "8"))))
     with cf.ThreadPoolExecutor(jobs) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
+        objs = list(ex.map(lambda u: _compile(u, verbose), UNITS))
     tmp = LIB + ".tmp"
     cmd = [_hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs
     if verbose:

@@ -14,38 +14,56 @@ bool is_layout(int v) { return v == GBA_ROW_MAJOR || v == GBA_COL_MAJOR; }
 
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
-gba_status validate_gemm(int la, int lb, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
-                         const void *B, int64_t ldb, const void *bias, const void *C, int64_t ldc,
-                         int act, int accum)
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+bool has_second(const gba_fused_desc &d) { return d.second != GBA_SECOND_NONE; }
+
+// Host-side validation of a request (include/gba.h states the rules).
+gba_status validate(const gba_fused_desc &d)
 {
-    if (!is_layout(la) || !is_layout(lb)) return GBA_EINVAL;
-    if (act != GBA_ACT_NONE && act != GBA_ACT_RELU) return GBA_EINVAL;
-    if (accum != GBA_ACC_F32 && accum != GBA_ACC_F16) return GBA_EINVAL;
-    if (M < 0 || N < 0 || K < 0 || lda < 0 || ldb < 0 || ldc < 0) return GBA_EINVAL;
-    if (M > INT_MAX || N > INT_MAX || K > INT_MAX) return GBA_EUNSUPPORTED;
-    if (M == 0 || N == 0) return GBA_OK;
-    if (C == nullptr || ldc < N) return GBA_EINVAL;
-    if (K > 0) {
-        if (A == nullptr || B == nullptr) return GBA_EINVAL;
-        if (lda < (la == GBA_ROW_MAJOR ? K : M)) return GBA_EINVAL;
-        if (ldb < (lb == GBA_ROW_MAJOR ? N : K)) return GBA_EINVAL;
+    if (!is_layout(d.layoutA) || !is_layout(d.layoutB)) return GBA_EINVAL;
+    if (d.act < GBA_ACT_NONE || d.act > GBA_ACT_TANH) return GBA_EINVAL;
+    if (d.accum != GBA_ACC_F32 && d.accum != GBA_ACC_F16) return GBA_EINVAL;
+    if (d.prologue != GBA_PRO_NONE && d.prologue != GBA_PRO_RELU) return GBA_EINVAL;
+    if (d.second < GBA_SECOND_NONE || d.second > GBA_SECOND_SUB) return GBA_EINVAL;
+    if (d.bias_kind < GBA_BIAS_NONE || d.bias_kind > GBA_BIAS_FULL) return GBA_EINVAL;
+    if (d.bias_op != GBA_OP_ADD && d.bias_op != GBA_OP_SUB) return GBA_EINVAL;
+    if (d.tile_id >= NUM_TILES) return GBA_EINVAL;
+    const bool two = has_second(d);
+    if (d.M < 0 || d.N < 0 || d.K < 0 || d.lda < 0 || d.ldb < 0 || d.ldc < 0) return GBA_EINVAL;
+    if (two && (d.K2 < 0 || d.ldp < 0 || d.ldq < 0)) return GBA_EINVAL;
+    if (d.bias_kind == GBA_BIAS_FULL && d.ldbias < 0) return GBA_EINVAL;
+    if (d.M > INT_MAX || d.N > INT_MAX || d.K > INT_MAX || (two && d.K2 > INT_MAX))
+        return GBA_EUNSUPPORTED;
+    if (d.M == 0 || d.N == 0) return GBA_OK;
+    if (d.C == nullptr || d.ldc < d.N) return GBA_EINVAL;
+    const bool rowA = d.layoutA == GBA_ROW_MAJOR, rowB = d.layoutB == GBA_ROW_MAJOR;
+    if (d.K > 0) {
+        if (d.A == nullptr || d.B == nullptr) return GBA_EINVAL;
+        if (d.lda < (rowA ? d.K : d.M) || d.ldb < (rowB ? d.N : d.K)) return GBA_EINVAL;
     }
-    if (!aligned(A, 2) || !aligned(B, 2) || !aligned(C, 2) || !aligned(bias, 2))
+    if (two && d.K2 > 0) {
+        if (d.P == nullptr || d.Q == nullptr) return GBA_EINVAL;
+        if (d.ldp < (rowA ? d.K2 : d.M) || d.ldq < (rowB ? d.N : d.K2)) return GBA_EINVAL;
+    }
+    if (d.bias_kind != GBA_BIAS_NONE && d.bias == nullptr) return GBA_EINVAL;
+    if (d.bias_kind == GBA_BIAS_FULL && d.ldbias < d.N) return GBA_EINVAL;
+    const bool with_bias = d.bias_kind != GBA_BIAS_NONE;
+    if (!aligned(d.A, 2) || !aligned(d.B, 2) || !aligned(d.C, 2) || (with_bias && !aligned(d.bias, 2)) ||
+        (two && (!aligned(d.P, 2) || !aligned(d.Q, 2))))
         return GBA_EUNSUPPORTED;
     return GBA_OK;
 }
 
-int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
-
 bool tile_fits(int tile, int64_t M, int64_t N) { return M >= TILES[tile].bm && N >= TILES[tile].bn; }
 
-// Tile choice by problem shape.  With enough output tiles, the largest block
-// tile that fits inside the problem and still yields a workgroup for each
-// of the 256 compute units.  With few output tiles and a long reduction,
-// intra-workgroup split-K over a small tile (fp32 accumulation only): its
-// four k-groups and four-stage copies keep the memory system busy where
-// the plain tiles would leave most compute units idle.  Otherwise the tile
-// with the most workgroups.
+// Tile choice by problem shape (K is the total reduction length).  With
+// enough output tiles, the largest block tile that fits inside the problem
+// and still yields a workgroup for each of the 256 compute units.  With few
+// output tiles and a long reduction, intra-workgroup split-K over a small
+// tile (fp32 accumulation only): its four k-groups and four-stage copies
+// keep the memory system busy where the plain tiles would leave most
+// compute units idle.  Otherwise the tile with the most workgroups.
 int select_tile(int64_t M, int64_t N, int64_t K, int accum)
 {
     const int64_t CUS = 256;
@@ -63,60 +81,107 @@ constexpr int64_t FAST_MAX_LD = int64_t(1) << 21;
 
 // The fast path needs every 16-byte chunk of every operand wholly inside or
 // wholly outside the matrix.
-bool fast_path_ok(int la, int lb, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
-                  const void *B, int64_t ldb, const void *bias, const void *C, int64_t ldc)
+bool fast_path_ok(const gba_fused_desc &d)
 {
-    if (!aligned(A, 16) || !aligned(B, 16) || !aligned(C, 16) || !aligned(bias, 16)) return false;
-    if (lda % 8 || ldb % 8 || ldc % 8 || lda >= FAST_MAX_LD || ldb >= FAST_MAX_LD) return false;
-    if (N % 8) return false;
-    if ((la == GBA_ROW_MAJOR ? K : M) % 8) return false;
-    if ((lb == GBA_COL_MAJOR ? K : N) % 8) return false;
+    const bool two = has_second(d), rowA = d.layoutA == GBA_ROW_MAJOR, colB = d.layoutB == GBA_COL_MAJOR;
+    if (!aligned(d.A, 16) || !aligned(d.B, 16) || !aligned(d.C, 16)) return false;
+    if (d.bias_kind != GBA_BIAS_NONE && !aligned(d.bias, 16)) return false;
+    if (d.lda % 8 || d.ldb % 8 || d.ldc % 8 || d.lda >= FAST_MAX_LD || d.ldb >= FAST_MAX_LD) return false;
+    if (d.bias_kind == GBA_BIAS_FULL && d.ldbias % 8) return false;
+    if (d.N % 8 || (rowA ? d.K : d.M) % 8 || (colB ? d.K : d.N) % 8) return false;
+    if (two) {
+        if (!aligned(d.P, 16) || !aligned(d.Q, 16)) return false;
+        if (d.ldp % 8 || d.ldq % 8 || d.ldp >= FAST_MAX_LD || d.ldq >= FAST_MAX_LD) return false;
+        if ((rowA ? d.K2 : d.M) % 8 || (colB ? d.K2 : d.N) % 8) return false;
+    }
     return true;
 }
 
-const LayoutTable &table_for(int la, int lb)
+template <int LA, int LB>
+const LayoutTable &variant_table(bool pro, bool dual)
 {
-    if (la == GBA_ROW_MAJOR) return lb == GBA_ROW_MAJOR ? table_RR() : table_RC();
-    return lb == GBA_ROW_MAJOR ? table_CR() : table_CC();
+    if (pro) return dual ? layout_table<LA, LB, true, true>() : layout_table<LA, LB, true, false>();
+    return dual ? layout_table<LA, LB, false, true>() : layout_table<LA, LB, false, false>();
 }
 
-gba_status run_gemm(int la, int lb, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
-                    const void *B, int64_t ldb, const void *bias, void *C, int64_t ldc, int act,
-                    int accum, int tile_id, hipStream_t stream)
+const LayoutTable &table_for(int la, int lb, bool pro, bool dual)
 {
-    if (tile_id >= NUM_TILES) return GBA_EINVAL;
-    gba_status st = validate_gemm(la, lb, M, N, K, A, lda, B, ldb, bias, C, ldc, act, accum);
-    if (st != GBA_OK || M == 0 || N == 0) return st;
+    if (la == GBA_ROW_MAJOR)
+        return lb == GBA_ROW_MAJOR ? variant_table<ROW, ROW>(pro, dual) : variant_table<ROW, COL>(pro, dual);
+    return lb == GBA_ROW_MAJOR ? variant_table<COL, ROW>(pro, dual) : variant_table<COL, COL>(pro, dual);
+}
+
+gba_status run_fused(const gba_fused_desc &d, hipStream_t stream)
+{
+    gba_status st = validate(d);
+    if (st != GBA_OK || d.M == 0 || d.N == 0) return st;
+    const bool two = has_second(d);
+    const int64_t ktot = d.K + (two ? d.K2 : 0);
 
     // A requested tile that is larger than the problem is replaced by the
     // library's choice; problems smaller than every tile take the general path.
-    const bool tile_ok = tile_id >= 0 && tile_fits(tile_id, M, N) &&
-                         !(accum == GBA_ACC_F16 && TILES[tile_id].sk > 1);
-    int tile = tile_ok ? tile_id : select_tile(M, N, K, accum);
-    const bool fast = tile >= 0 && fast_path_ok(la, lb, M, N, K, A, lda, B, ldb, bias, C, ldc);
+    const bool tile_ok = d.tile_id >= 0 && tile_fits(d.tile_id, d.M, d.N) &&
+                         !(d.accum == GBA_ACC_F16 && TILES[d.tile_id].sk > 1);
+    int tile = tile_ok ? d.tile_id : select_tile(d.M, d.N, ktot, d.accum);
+    const bool fast = tile >= 0 && fast_path_ok(d);
     if (!fast) tile = -1;
     const TileCfg cfg = fast ? TILES[tile] : GENERIC_TILE;
 
     GemmArgs a;
-    a.A = static_cast<const _Float16 *>(A);
-    a.B = static_cast<const _Float16 *>(B);
-    a.bias = static_cast<const _Float16 *>(bias);
-    a.C = static_cast<_Float16 *>(C);
-    a.lda = lda;
-    a.ldb = ldb;
-    a.ldc = ldc;
-    a.M = (int)M;
-    a.N = (int)N;
-    a.K = (int)K;
-    a.relu = act == GBA_ACT_RELU;
-    a.tiles_m = (int)ceil_div(M, cfg.bm);
-    a.tiles_n = (int)ceil_div(N, cfg.bn);
+    a.A = static_cast<const _Float16 *>(d.A);
+    a.B = static_cast<const _Float16 *>(d.B);
+    a.P = two ? static_cast<const _Float16 *>(d.P) : nullptr;
+    a.Q = two ? static_cast<const _Float16 *>(d.Q) : nullptr;
+    a.bias = d.bias_kind == GBA_BIAS_NONE ? nullptr : static_cast<const _Float16 *>(d.bias);
+    a.C = static_cast<_Float16 *>(d.C);
+    a.lda = d.lda;
+    a.ldb = d.ldb;
+    a.ldp = two ? d.ldp : 0;
+    a.ldq = two ? d.ldq : 0;
+    a.ldc = d.ldc;
+    a.ldbias = d.bias_kind == GBA_BIAS_FULL ? d.ldbias : 0;
+    a.M = (int)d.M;
+    a.N = (int)d.N;
+    a.K = (int)d.K;
+    a.K2 = two ? (int)d.K2 : 0;
+    a.act = d.act;
+    a.bias_kind = d.bias_kind;
+    a.bias_sign = d.bias_op == GBA_OP_SUB ? -1.f : 1.f;
+    a.sub = d.second == GBA_SECOND_SUB;
+    a.tiles_m = (int)ceil_div(d.M, cfg.bm);
+    a.tiles_n = (int)ceil_div(d.N, cfg.bn);
     if ((int64_t)a.tiles_m * a.tiles_n > INT_MAX) return GBA_EUNSUPPORTED;
 
-    const LayoutTable &tab = table_for(la, lb);
-    const int acc16 = accum == GBA_ACC_F16;
+    const LayoutTable &tab = table_for(d.layoutA, d.layoutB, d.prologue == GBA_PRO_RELU, two);
+    const int acc16 = d.accum == GBA_ACC_F16;
     LaunchFn fn = fast ? tab.fast[tile][acc16] : tab.generic[acc16];
     return fn(a, stream) == hipSuccess ? GBA_OK : GBA_EHIP;
+}
+
+// The request of gemm_bias_act: one product, no prologue, row bias if any.
+gba_fused_desc single_product(gba_layout la, gba_layout lb, int64_t M, int64_t N, int64_t K,
+                              const void *A, int64_t lda, const void *B, int64_t ldb, const void *bias,
+                              void *C, int64_t ldc, gba_act act, gba_acc accum, int tile_id)
+{
+    gba_fused_desc d;
+    gba_fused_desc_init(&d);
+    d.layoutA = la;
+    d.layoutB = lb;
+    d.M = M;
+    d.N = N;
+    d.K = K;
+    d.A = A;
+    d.lda = lda;
+    d.B = B;
+    d.ldb = ldb;
+    d.bias_kind = bias ? GBA_BIAS_ROW : GBA_BIAS_NONE;
+    d.bias = bias;
+    d.act = act;
+    d.accum = accum;
+    d.C = C;
+    d.ldc = ldc;
+    d.tile_id = tile_id;
+    return d;
 }
 
 // ---------------------------------------------------------------------------
@@ -169,6 +234,31 @@ __global__ void __launch_bounds__(256) relu_kernel(_Float16 *C, int64_t ldc, int
     }
 }
 
+template <bool VEC>
+__global__ void __launch_bounds__(256) add_kernel(_Float16 *C, int64_t ldc, const _Float16 *X, int64_t ldx,
+                                                  int M, int N)
+{
+    const int64_t nch = (N + 7) / 8;
+    const int64_t total = (int64_t)M * nch;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = idx / nch;
+        const int j = (int)(idx - i * nch) * 8;
+        _Float16 *row = C + i * ldc + j;
+        const _Float16 *xrow = X + i * ldx + j;
+        if (VEC && j + 8 <= N) {
+            h8 c = *reinterpret_cast<const h8 *>(row);
+            const h8 x = *reinterpret_cast<const h8 *>(xrow);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) c[e] = (_Float16)((float)c[e] + (float)x[e]);
+            *reinterpret_cast<h8 *>(row) = c;
+        } else {
+            for (int e = 0; e < 8 && j + e < N; ++e)
+                row[e] = (_Float16)((float)row[e] + (float)xrow[e]);
+        }
+    }
+}
+
 unsigned pointwise_grid(int64_t M, int64_t N)
 {
     int64_t chunks = M * ((N + 7) / 8);
@@ -192,13 +282,34 @@ gba_status validate_pointwise(int64_t M, int64_t N, const void *C, int64_t ldc, 
 
 using namespace gba;
 
+extern "C" void gba_fused_desc_init(gba_fused_desc *desc)
+{
+    if (desc == nullptr) return;
+    *desc = gba_fused_desc{};
+    desc->layoutA = GBA_ROW_MAJOR;
+    desc->layoutB = GBA_ROW_MAJOR;
+    desc->prologue = GBA_PRO_NONE;
+    desc->second = GBA_SECOND_NONE;
+    desc->bias_kind = GBA_BIAS_NONE;
+    desc->bias_op = GBA_OP_ADD;
+    desc->act = GBA_ACT_NONE;
+    desc->accum = GBA_ACC_F32;
+    desc->tile_id = -1;
+}
+
+extern "C" gba_status gba_fused_gemm(const gba_fused_desc *desc, gba_stream_t stream)
+{
+    if (desc == nullptr) return GBA_EINVAL;
+    return run_fused(*desc, reinterpret_cast<hipStream_t>(stream));
+}
+
 extern "C" gba_status gemm_bias_act(gba_layout layoutA, gba_layout layoutB, int64_t M, int64_t N,
                                     int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
                                     const void *bias, void *C, int64_t ldc, gba_act act,
                                     gba_acc accum, gba_stream_t stream)
 {
-    return run_gemm(layoutA, layoutB, M, N, K, A, lda, B, ldb, bias, C, ldc, act, accum, -1,
-                    reinterpret_cast<hipStream_t>(stream));
+    return run_fused(single_product(layoutA, layoutB, M, N, K, A, lda, B, ldb, bias, C, ldc, act, accum, -1),
+                     reinterpret_cast<hipStream_t>(stream));
 }
 
 extern "C" gba_status gemm_bias_act_tile(gba_layout layoutA, gba_layout layoutB, int64_t M,
@@ -207,8 +318,9 @@ extern "C" gba_status gemm_bias_act_tile(gba_layout layoutA, gba_layout layoutB,
                                          int64_t ldc, gba_act act, gba_acc accum, int tile_id,
                                          gba_stream_t stream)
 {
-    return run_gemm(layoutA, layoutB, M, N, K, A, lda, B, ldb, bias, C, ldc, act, accum, tile_id,
-                    reinterpret_cast<hipStream_t>(stream));
+    return run_fused(
+        single_product(layoutA, layoutB, M, N, K, A, lda, B, ldb, bias, C, ldc, act, accum, tile_id),
+        reinterpret_cast<hipStream_t>(stream));
 }
 
 extern "C" int gba_num_tiles(void) { return NUM_TILES; }
@@ -263,6 +375,24 @@ extern "C" gba_status gba_relu_f16(int64_t M, int64_t N, void *C, int64_t ldc, g
         hipLaunchKernelGGL(relu_kernel<true>, grid, block, 0, s, c, ldc, (int)M, (int)N);
     else
         hipLaunchKernelGGL(relu_kernel<false>, grid, block, 0, s, c, ldc, (int)M, (int)N);
+    return hipGetLastError() == hipSuccess ? GBA_OK : GBA_EHIP;
+}
+
+extern "C" gba_status gba_add_f16(int64_t M, int64_t N, void *C, int64_t ldc, const void *X, int64_t ldx,
+                                  gba_stream_t stream)
+{
+    gba_status st = validate_pointwise(M, N, C, ldc, X, true);
+    if (st != GBA_OK || M == 0 || N == 0) return st;
+    if (ldx < N) return GBA_EINVAL;
+    const bool vec = aligned(C, 16) && aligned(X, 16) && ldc % 8 == 0 && ldx % 8 == 0;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    dim3 grid(pointwise_grid(M, N)), block(256);
+    _Float16 *c = static_cast<_Float16 *>(C);
+    const _Float16 *x = static_cast<const _Float16 *>(X);
+    if (vec)
+        hipLaunchKernelGGL(add_kernel<true>, grid, block, 0, s, c, ldc, x, ldx, (int)M, (int)N);
+    else
+        hipLaunchKernelGGL(add_kernel<false>, grid, block, 0, s, c, ldc, x, ldx, (int)M, (int)N);
     return hipGetLastError() == hipSuccess ? GBA_OK : GBA_EHIP;
 }
 

@@ -14,17 +14,26 @@ typedef float f16v __attribute__((ext_vector_type(16)));
 typedef int i4 __attribute__((ext_vector_type(4)));
 
 enum { ROW = 0, COL = 1 };
+enum { ACT_NONE = 0, ACT_RELU = 1, ACT_SIGMOID = 2, ACT_TANH = 3 };
+enum { BIAS_NONE = 0, BIAS_ROW = 1, BIAS_FULL = 2 };
 
 // Kernel arguments: operands as the C ABI describes them (A(i,k), B(k,j) per
-// layout, C row-major), the activation switch and the output tile grid.
+// layout, C row-major), the optional second product P.Q (same layouts as A
+// and B, reduction length K2; read only by kernels built for two products),
+// the epilogue's bias and activation, and the output tile grid.
 struct GemmArgs {
     const _Float16 *A;
     const _Float16 *B;
-    const _Float16 *bias;  // may be null
+    const _Float16 *P;
+    const _Float16 *Q;
+    const _Float16 *bias;  // null when bias_kind == BIAS_NONE
     _Float16 *C;
-    int64_t lda, ldb, ldc;
-    int M, N, K;
-    int relu;
+    int64_t lda, ldb, ldp, ldq, ldc, ldbias;
+    int M, N, K, K2;
+    int act;               // ACT_*
+    int bias_kind;         // BIAS_*: bias[j] or bias[i*ldbias + j]
+    float bias_sign;       // +1: add the bias, -1: subtract it
+    int sub;               // nonzero: C = A.B - P.Q instead of A.B + P.Q
     int tiles_m, tiles_n;
 };
 
@@ -34,6 +43,40 @@ __device__ __forceinline__ h8 zero_h8()
 #pragma unroll
     for (int e = 0; e < 8; ++e) z[e] = (_Float16)0.0f;
     return z;
+}
+
+// max(x, 0) on eight fp16 values (the ReLU of a prologue).
+__device__ __forceinline__ h8 relu_h8(h8 v) { return __builtin_elementwise_max(v, zero_h8()); }
+
+// tanh from its odd Taylor series near 0 (|x| < 1/16, where the next term
+// is below 2^-28 relative) and from tanh|x| = (1 - e) / (1 + e),
+// e = exp(-2|x|), elsewhere.
+__device__ __forceinline__ float tanh_f32(float x)
+{
+    const float ax = __builtin_fabsf(x);
+    const float x2 = x * x;
+    const float series = x * (1.f + x2 * (-1.f / 3.f + x2 * (2.f / 15.f)));
+    const float e = __expf(-2.f * ax);
+    const float t = (1.f - e) * __builtin_amdgcn_rcpf(1.f + e);
+    const float big = __builtin_copysignf(t, x);
+    return ax < 0.0625f ? series : big;
+}
+
+// The epilogue's activation on NV values; act is uniform across the grid.
+// Sigmoid is 1 / (1 + exp(-x)).
+template <int NV>
+__device__ __forceinline__ void activate(int act, float (&x)[NV])
+{
+    if (act == ACT_RELU) {
+#pragma unroll
+        for (int e = 0; e < NV; ++e) x[e] = x[e] > 0.f ? x[e] : 0.f;
+    } else if (act == ACT_SIGMOID) {
+#pragma unroll
+        for (int e = 0; e < NV; ++e) x[e] = __builtin_amdgcn_rcpf(1.f + __expf(-x[e]));
+    } else if (act == ACT_TANH) {
+#pragma unroll
+        for (int e = 0; e < NV; ++e) x[e] = tanh_f32(x[e]);
+    }
 }
 
 // Map the hardware workgroup id to a (tile_m, tile_n) pair.  Workgroups are

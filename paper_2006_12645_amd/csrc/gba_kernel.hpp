@@ -216,8 +216,11 @@ __device__ __forceinline__ void sched_slice()
 }
 
 // Register-staged copy of one operand tile (any layout): global -> registers
-// during one step, registers -> LDS during the next.
-template <int R, int NT, bool KCONT>
+// during one step, registers -> LDS during the next.  RELU: the prologue's
+// ReLU is applied to the staged values between the two copies, so LDS holds
+// relu(X) and the footprint is that of the plain operand (Pointwise
+// Operations in Prologue subsection).
+template <int R, int NT, bool KCONT, bool RELU>
 struct RegCopy {
     using Stage = FastStage<R, NT, KCONT>;
     static constexpr int NLOAD = Stage::NREG;                   // global loads per step
@@ -226,7 +229,14 @@ struct RegCopy {
     __device__ __forceinline__ void init(int64_t ld, int tid) { st.init(ld, tid); }
     __device__ __forceinline__ void dma(__amdgpu_buffer_rsrc_t, char *, int) {}
     __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, int kleft) { st.load(rs, kleft); }
-    __device__ __forceinline__ void write(char *stage) const { st.store(stage); }
+    __device__ __forceinline__ void write(char *stage)
+    {
+        if constexpr (RELU) {
+#pragma unroll
+            for (int i = 0; i < Stage::NREG; ++i) st.v[i] = relu_h8(st.v[i]);
+        }
+        st.store(stage);
+    }
 };
 
 // Direct global -> LDS copy of a reduction-contiguous operand tile with the
@@ -279,7 +289,7 @@ struct DmaCopy {
         }
     }
     __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t, int) {}
-    __device__ __forceinline__ void write(char *) const {}
+    __device__ __forceinline__ void write(char *) {}
 };
 
 // SK > 1: intra-workgroup split-K (Split-K subsection): the workgroup holds
@@ -292,7 +302,16 @@ struct DmaCopy {
 // before the step is multiplied, so small tiles that cannot cover the
 // memory latency with work hide it with depth.  Register-staged operands
 // keep two stages.
-template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool DMA>
+// PRO: the prologue's ReLU on the left operand of every product (Pointwise
+// Operations in Prologue subsection): applied to the staged registers when
+// that operand is register-staged, else to its MFMA fragments as they leave
+// LDS; either way LDS holds one copy of the operand.
+// DUAL: a second product P.Q of the same output shape is accumulated into
+// the same registers after A.B (Matmuls with Pointwise Epilogue
+// subsection): the reduction runs over A.B's K steps and then over P.Q's K2
+// steps, and only the sum (or difference) leaves the kernel.
+template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool DMA,
+          bool PRO, bool DUAL>
 __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs p)
 {
     constexpr int NTG = 64 * WM * WN;         // threads per k-group
@@ -332,39 +351,12 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
     const int mc = m0 + BM <= p.M ? m0 : p.M - BM;
     const int nc = n0 + BN <= p.N ? n0 : p.N - BN;
 
-    using CopyA = std::conditional_t<DMA && LA == ROW, DmaCopy<BM, NTG>, RegCopy<BM, NTG, LA == ROW>>;
-    using CopyB = std::conditional_t<DMA && LB == COL, DmaCopy<BN, NTG>, RegCopy<BN, NTG, LB == COL>>;
+    constexpr bool DMA_A = DMA && LA == ROW;
+    constexpr bool FRAG_RELU = PRO && DMA_A;  // ReLU on fragments (no register stage)
+    using CopyA = std::conditional_t<DMA_A, DmaCopy<BM, NTG>, RegCopy<BM, NTG, LA == ROW, PRO>>;
+    using CopyB = std::conditional_t<DMA && LB == COL, DmaCopy<BN, NTG>, RegCopy<BN, NTG, LB == COL, false>>;
     CopyA ca;
     CopyB cb;
-    ca.init(p.lda, gtid);
-    cb.init(p.ldb, gtid);
-
-    // Resource of the step starting at reduction index k0 for each operand.
-    auto rsrc_a = [&](int k0) {
-        if constexpr (LA == ROW) return make_rsrc(p.A + (int64_t)mc * p.lda + k0, MAX_RECORDS);
-        else return make_rsrc(p.A + (int64_t)k0 * p.lda + mc, MAX_RECORDS);
-    };
-    auto rsrc_b = [&](int k0) {
-        if constexpr (LB == COL) return make_rsrc(p.B + (int64_t)nc * p.ldb + k0, MAX_RECORDS);
-        else return make_rsrc(p.B + (int64_t)k0 * p.ldb + nc, MAX_RECORDS);
-    };
-    const int nk = (p.K + SK * BK - 1) / (SK * BK);
-
-    // Copies of step s (this k-group's slab): direct-to-LDS operands into
-    // `stage`, the others into their staging registers.  Steps past the
-    // last one re-fetch the last step (into a stage nobody reads again), so
-    // every step of the loop below has the same shape.  A slab starting at
-    // or beyond K reads as zeros.
-    auto copy_step = [&](int s, char *stage) {
-        const int k0 = ((s < nk ? s : nk - 1) * SK + grp) * BK;
-        const int kleft = p.K - k0;
-        const auto ra = rsrc_a(k0);
-        const auto rb = rsrc_b(k0);
-        ca.dma(ra, stage, kleft);
-        cb.dma(rb, stage + BM * ROWB, kleft);
-        ca.load(ra, kleft);
-        cb.load(rb, kleft);
-    };
 
     // Fragment byte offsets inside a stage for each 16-deep slice ks; blocks
     // further along differ by 32 rows = 4096 bytes.
@@ -396,6 +388,12 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
         for (int t = 0; t < TN; ++t) fp[buf][t] = *reinterpret_cast<const h8 *>(stage + offp[ks] + t * 32 * ROWB);
     };
     auto mfmas = [&](int buf) {
+        if constexpr (FRAG_RELU) {
+            // the prologue's ReLU, once per fragment, right before its use
+            // (so the fragment read in flight is not waited for early)
+#pragma unroll
+            for (int s = 0; s < TM; ++s) fq[buf][s] = relu_h8(fq[buf][s]);
+        }
 #pragma unroll
         for (int t = 0; t < TN; ++t)
 #pragma unroll
@@ -414,6 +412,12 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
                     for (int e = 0; e < 16; ++e) acc[t][s][e] = (float)(_Float16)acc[t][s][e];
         }
     };
+    auto negate_acc = [&]() {
+#pragma unroll
+        for (int t = 0; t < TN; ++t)
+#pragma unroll
+            for (int s = 0; s < TM; ++s) acc[t][s] = -acc[t][s];
+    };
 
     // Instruction interleaving hints for the scheduler: each MFMA is paired
     // with the fragment read (DS read), staging write (DS write) or global
@@ -422,67 +426,116 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
     constexpr int NR = TM + TN;           // fragment reads per slice
     constexpr int NW = CopyA::NWRITE + CopyB::NWRITE;
     constexpr int NL = CopyA::NLOAD + CopyB::NLOAD;
-
-    // Prologue: step 0 into LDS stage 0 and step 1 under way (into stage 1
-    // or the staging registers), then the first fragments of step 0.
-    char *const mine = lds + grp * SUB;   // this k-group's sub-stage of stage 0
-    if (nk > 0) {
-        copy_step(0, mine);
-        ca.write(mine);
-        cb.write(mine + BM * ROWB);
-#pragma unroll
-        for (int s = 1; s < NS; ++s) copy_step(s, mine + s * STAGE);
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        read_frags(0, mine, 0);
-    }
     // Global loads still allowed in flight at the barrier of step kt: the
     // copies of steps kt+2 .. kt+NS-1; step kt+1 must have landed.
     constexpr int VM_AT_BARRIER = (NS - 2) * NL;
+    char *const mine = lds + grp * SUB;   // this k-group's sub-stage of stage 0
 
-    // One reduction step.  On entry LDS stage `cur` holds step kt, step kt+1
-    // is under way (into `nxt` or the staging registers) and fq/fp[0] hold
-    // slice 0 of step kt.
-    for (int kt = 0; kt < nk; ++kt) {
-        char *cur = mine + (kt & (NS - 1)) * STAGE;
-        char *nxt = mine + ((kt + 1) & (NS - 1)) * STAGE;
-        // slice 0 (fragments of slice 1 in flight)
-        read_frags(1, cur, 1);
-        mfmas(0);
-        sched_slice<NM, NR, 0, 0>();
-        // slice 1
-        read_frags(0, cur, 2);
-        mfmas(1);
-        round16();
-        sched_slice<NM, NR, 0, 0>();
-        // slice 2, plus the register-staged writes of step kt+1
-        read_frags(1, cur, 3);
-        mfmas(0);
-        ca.write(nxt);
-        cb.write(nxt + BM * ROWB);
-        sched_slice<NM, NR, 0x200, NW>();
-        // Step kt+1 complete in LDS for every wave; every read of `cur` done.
-        if constexpr (VM_AT_BARRIER == 0) {
+    // One pass of the pipelined reduction per product: A.B, then (DUAL)
+    // P.Q on top of it.  C - R is formed as -((-C) + R): negating the
+    // running sum is exact and rounding is symmetric, so this equals
+    // subtracting every product of R.
+#pragma unroll 1
+    for (int seg = 0; seg < (DUAL ? 2 : 1); ++seg) {
+        const _Float16 *const X = seg == 0 ? p.A : p.P;
+        const _Float16 *const Y = seg == 0 ? p.B : p.Q;
+        const int64_t ldx = seg == 0 ? p.lda : p.ldp;
+        const int64_t ldy = seg == 0 ? p.ldb : p.ldq;
+        const int Kseg = seg == 0 ? p.K : p.K2;
+        if (seg == 1) {
+            // every wave is done with the first product's LDS stages (and
+            // its trailing copies have landed) before they are refilled
+            __syncthreads();
+            if (p.sub) negate_acc();
+        }
+        ca.init(ldx, gtid);
+        cb.init(ldy, gtid);
+
+        // Resource of the step starting at reduction index k0 for each operand.
+        auto rsrc_a = [&](int k0) {
+            if constexpr (LA == ROW) return make_rsrc(X + (int64_t)mc * ldx + k0, MAX_RECORDS);
+            else return make_rsrc(X + (int64_t)k0 * ldx + mc, MAX_RECORDS);
+        };
+        auto rsrc_b = [&](int k0) {
+            if constexpr (LB == COL) return make_rsrc(Y + (int64_t)nc * ldy + k0, MAX_RECORDS);
+            else return make_rsrc(Y + (int64_t)k0 * ldy + nc, MAX_RECORDS);
+        };
+        const int nk = (Kseg + SK * BK - 1) / (SK * BK);
+
+        // Copies of step s (this k-group's slab): direct-to-LDS operands into
+        // `stage`, the others into their staging registers.  Steps past the
+        // last one re-fetch the last step (into a stage nobody reads again), so
+        // every step of the loop below has the same shape.  A slab starting at
+        // or beyond K reads as zeros.
+        auto copy_step = [&](int s, char *stage) {
+            const int k0 = ((s < nk ? s : nk - 1) * SK + grp) * BK;
+            const int kleft = Kseg - k0;
+            const auto ra = rsrc_a(k0);
+            const auto rb = rsrc_b(k0);
+            ca.dma(ra, stage, kleft);
+            cb.dma(rb, stage + BM * ROWB, kleft);
+            ca.load(ra, kleft);
+            cb.load(rb, kleft);
+        };
+
+        // Prologue: step 0 into LDS stage 0 and step 1 under way (into stage 1
+        // or the staging registers), then the first fragments of step 0.
+        if (nk > 0) {
+            copy_step(0, mine);
+            ca.write(mine);
+            cb.write(mine + BM * ROWB);
+#pragma unroll
+            for (int s = 1; s < NS; ++s) copy_step(s, mine + s * STAGE);
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
-        } else {
-            __builtin_amdgcn_sched_barrier(0);
-            wait_vm_lgkm0<VM_AT_BARRIER>();
-            __builtin_amdgcn_s_barrier();
-            __builtin_amdgcn_sched_barrier(0);
+            read_frags(0, mine, 0);
         }
-        // slice 3, plus the first fragments of step kt+1 and the copies of
-        // step kt+NS (into `cur`, now free)
-        read_frags(0, nxt, 0);
-        mfmas(1);
-        round16();
-        copy_step(kt + NS, cur);
-        sched_slice<NM, NR, 0x020, NL>();
-    }
 
-    // Drain the trailing (unused) copies: nothing may still be writing LDS
-    // when it is reused below or released.
-    __builtin_amdgcn_s_waitcnt(0);
+        // One reduction step.  On entry LDS stage `cur` holds step kt, step kt+1
+        // is under way (into `nxt` or the staging registers) and fq/fp[0] hold
+        // slice 0 of step kt.
+        for (int kt = 0; kt < nk; ++kt) {
+            char *cur = mine + (kt & (NS - 1)) * STAGE;
+            char *nxt = mine + ((kt + 1) & (NS - 1)) * STAGE;
+            // slice 0 (fragments of slice 1 in flight)
+            read_frags(1, cur, 1);
+            mfmas(0);
+            sched_slice<NM, NR, 0, 0>();
+            // slice 1
+            read_frags(0, cur, 2);
+            mfmas(1);
+            round16();
+            sched_slice<NM, NR, 0, 0>();
+            // slice 2, plus the register-staged writes of step kt+1
+            read_frags(1, cur, 3);
+            mfmas(0);
+            ca.write(nxt);
+            cb.write(nxt + BM * ROWB);
+            sched_slice<NM, NR, 0x200, NW>();
+            // Step kt+1 complete in LDS for every wave; every read of `cur` done.
+            if constexpr (VM_AT_BARRIER == 0) {
+                __builtin_amdgcn_s_waitcnt(0);
+                __syncthreads();
+            } else {
+                __builtin_amdgcn_sched_barrier(0);
+                wait_vm_lgkm0<VM_AT_BARRIER>();
+                __builtin_amdgcn_s_barrier();
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            // slice 3, plus the first fragments of step kt+1 and the copies of
+            // step kt+NS (into `cur`, now free)
+            read_frags(0, nxt, 0);
+            mfmas(1);
+            round16();
+            copy_step(kt + NS, cur);
+            sched_slice<NM, NR, 0x020, NL>();
+        }
+
+        // Drain the trailing (unused) copies: nothing may still be writing LDS
+        // when it is reused below or released.
+        __builtin_amdgcn_s_waitcnt(0);
+        if (seg == 1 && p.sub) negate_acc();
+    }
 
     if constexpr (SK > 1) {
         // Split-K: every k-group writes its partial tile to LDS (fp32, rows
@@ -519,38 +572,37 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
                     x[4 + e] += a1[e];
                 }
             }
-            if (p.bias != nullptr) {
-                const h8 bv = *reinterpret_cast<const h8 *>(p.bias + nc + j);
+            if (p.bias_kind != BIAS_NONE) {
+                const _Float16 *bp = p.bias_kind == BIAS_ROW ? p.bias + nc + j
+                                                             : p.bias + (int64_t)(mc + i) * p.ldbias + nc + j;
+                const h8 bv = *reinterpret_cast<const h8 *>(bp);
 #pragma unroll
-                for (int e = 0; e < 8; ++e) x[e] += (float)bv[e];
+                for (int e = 0; e < 8; ++e) x[e] += p.bias_sign * (float)bv[e];
             }
+            activate(p.act, x);
             h8 o;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                float v = x[e];
-                if (p.relu) v = v > 0.f ? v : 0.f;
-                o[e] = (_Float16)v;
-            }
+            for (int e = 0; e < 8; ++e) o[e] = (_Float16)x[e];
             if (mc + i >= m0 && nc + j >= n0)
                 *reinterpret_cast<h8 *>(p.C + (int64_t)(mc + i) * p.ldc + nc + j) = o;
         }
         return;
     }
 
-    // Epilogue on registers: + bias, ReLU, fp16, two 16-byte stores per lane
-    // per 32x32 block (each guarded so an output shared with a neighbouring
-    // tile is stored by its owner only).
+    // Epilogue on registers: +/- bias, activation, fp16, two 16-byte stores
+    // per lane per 32x32 block (each guarded so an output shared with a
+    // neighbouring tile is stored by its owner only).
 #pragma unroll
     for (int t = 0; t < TN; ++t) {
         const int j = nc + wn * WTN + 32 * t + 16 * hi;
         float b[16];
-        if (p.bias != nullptr) {
+        if (p.bias_kind == BIAS_ROW) {
             const h8 b0 = *reinterpret_cast<const h8 *>(p.bias + j);
             const h8 b1 = *reinterpret_cast<const h8 *>(p.bias + j + 8);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                b[e] = (float)b0[e];
-                b[8 + e] = (float)b1[e];
+                b[e] = p.bias_sign * (float)b0[e];
+                b[8 + e] = p.bias_sign * (float)b1[e];
             }
         } else {
 #pragma unroll
@@ -559,17 +611,25 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
 #pragma unroll
         for (int s = 0; s < TM; ++s) {
             const int i = mc + wm * WTM + 32 * s + l32;
+            float x[16];
+#pragma unroll
+            for (int e = 0; e < 16; ++e) x[e] = acc[t][s][e] + b[e];
+            if (p.bias_kind == BIAS_FULL) {
+                const _Float16 *bp = p.bias + (int64_t)i * p.ldbias + j;
+                const h8 b0 = *reinterpret_cast<const h8 *>(bp);
+                const h8 b1 = *reinterpret_cast<const h8 *>(bp + 8);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    x[e] += p.bias_sign * (float)b0[e];
+                    x[8 + e] += p.bias_sign * (float)b1[e];
+                }
+            }
+            activate(p.act, x);
             h8 o0, o1;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                float x0 = acc[t][s][e] + b[e];
-                float x1 = acc[t][s][8 + e] + b[8 + e];
-                if (p.relu) {
-                    x0 = x0 > 0.f ? x0 : 0.f;
-                    x1 = x1 > 0.f ? x1 : 0.f;
-                }
-                o0[e] = (_Float16)x0;
-                o1[e] = (_Float16)x1;
+                o0[e] = (_Float16)x[e];
+                o1[e] = (_Float16)x[8 + e];
             }
             if (i >= m0) {
                 _Float16 *dst = p.C + (int64_t)i * p.ldc + j;

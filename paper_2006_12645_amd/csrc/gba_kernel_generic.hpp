@@ -79,9 +79,11 @@ __device__ __forceinline__ h8 load8(const _Float16 *p, int lim)
 // Global -> register -> LDS copy of one operand tile of R rows (output rows
 // for A, output columns for B) by BK reduction indices.
 //   KCONT: the operand is reduction-contiguous in global memory.
+//   RELU: the prologue's ReLU is applied to the values on their way from
+//         the registers to LDS (Pointwise Operations in Prologue subsection).
 // X points at the operand, ld is its leading dimension, r0/k0 the tile origin,
 // rtot/ktot the extents.
-template <int R, int BK, int NT, bool KCONT, bool VEC>
+template <int R, int BK, int NT, bool KCONT, bool VEC, bool RELU>
 struct TileCopy16 {
     static constexpr int CHUNKS = R * BK / 8;                 // 16-byte chunks per tile
     static constexpr int KCH = BK / 8;                        // chunks per LDS row
@@ -123,8 +125,12 @@ struct TileCopy16 {
         }
     }
 
-    __device__ __forceinline__ void store(h8 *lds, int tid) const
+    __device__ __forceinline__ void store(h8 *lds, int tid)
     {
+        if constexpr (RELU) {
+#pragma unroll
+            for (int i = 0; i < NREG; ++i) v[i] = relu_h8(v[i]);
+        }
         if constexpr (KCONT) {
 #pragma unroll
             for (int p = 0; p < PER; ++p) {
@@ -155,7 +161,10 @@ struct TileCopy16 {
     }
 };
 
-template <int BM, int BN, int WM, int WN, int LA, int LB, bool ACC16, bool VEC>
+// PRO: ReLU prologue on the left operand of every product.  DUAL: a second
+// product P.Q is accumulated into the same registers after A.B (Matmuls
+// with Pointwise Epilogue subsection); C - R is formed as -((-C) + R).
+template <int BM, int BN, int WM, int WN, int LA, int LB, bool ACC16, bool VEC, bool PRO, bool DUAL>
 __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_generic(GemmArgs p)
 {
     constexpr int NT = 64 * WM * WN;
@@ -177,14 +186,20 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_generic(GemmArgs p
     tile_coords(blockIdx.x, gridDim.x, p.tiles_m, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
 
-    TileCopy16<BM, BK, NT, LA == ROW, VEC> ca;
-    TileCopy16<BN, BK, NT, LB == COL, VEC> cb;
+    TileCopy16<BM, BK, NT, LA == ROW, VEC, PRO> ca;
+    TileCopy16<BN, BK, NT, LB == COL, VEC, false> cb;
 
     f4 acc[TN][TM];
 #pragma unroll
     for (int t = 0; t < TN; ++t)
 #pragma unroll
         for (int s = 0; s < TM; ++s) acc[t][s] = f4{0.f, 0.f, 0.f, 0.f};
+    auto negate_acc = [&]() {
+#pragma unroll
+        for (int t = 0; t < TN; ++t)
+#pragma unroll
+            for (int s = 0; s < TM; ++s) acc[t][s] = -acc[t][s];
+    };
 
     // LDS read offsets (in chunks) of this lane's fragments, before the
     // k-chunk swizzle: row index and its swizzle value.
@@ -203,65 +218,78 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_generic(GemmArgs p
         swB[t] = swz16(r);
     }
 
-    const int nk = (p.K + BK - 1) / BK;
-    if (nk > 0) {
-        ca.load(p.A, p.lda, m0, 0, p.M, p.K, tid);
-        cb.load(p.B, p.ldb, n0, 0, p.N, p.K, tid);
-        ca.store(&lds[0][0], tid);
-        cb.store(&lds[0][BM * KCH], tid);
-        __syncthreads();
-    }
+#pragma unroll 1
+    for (int seg = 0; seg < (DUAL ? 2 : 1); ++seg) {
+        const _Float16 *const X = seg == 0 ? p.A : p.P;
+        const _Float16 *const Y = seg == 0 ? p.B : p.Q;
+        const int64_t ldx = seg == 0 ? p.lda : p.ldp;
+        const int64_t ldy = seg == 0 ? p.ldb : p.ldq;
+        const int Kseg = seg == 0 ? p.K : p.K2;
+        // (the last step of the previous pass ended with a barrier, so LDS
+        // is free to refill)
+        if (seg == 1 && p.sub) negate_acc();
 
-    for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        const bool more = kt + 1 < nk;
-        if (more) {
-            ca.load(p.A, p.lda, m0, (kt + 1) * BK, p.M, p.K, tid);
-            cb.load(p.B, p.ldb, n0, (kt + 1) * BK, p.N, p.K, tid);
+        const int nk = (Kseg + BK - 1) / BK;
+        if (nk > 0) {
+            ca.load(X, ldx, m0, 0, p.M, Kseg, tid);
+            cb.load(Y, ldy, n0, 0, p.N, Kseg, tid);
+            ca.store(&lds[0][0], tid);
+            cb.store(&lds[0][BM * KCH], tid);
+            __syncthreads();
         }
-        const h8 *L = &lds[cur][0];
+
+        for (int kt = 0; kt < nk; ++kt) {
+            const int cur = kt & 1;
+            const bool more = kt + 1 < nk;
+            if (more) {
+                ca.load(X, ldx, m0, (kt + 1) * BK, p.M, Kseg, tid);
+                cb.load(Y, ldy, n0, (kt + 1) * BK, p.N, Kseg, tid);
+            }
+            const h8 *L = &lds[cur][0];
 #pragma unroll
-        for (int ks = 0; ks < BK / 32; ++ks) {
-            const int c = ks * 4 + kq;
-            h8 fa[TM], fb[TN];
+            for (int ks = 0; ks < BK / 32; ++ks) {
+                const int c = ks * 4 + kq;
+                h8 fa[TM], fb[TN];
 #pragma unroll
-            for (int s = 0; s < TM; ++s) fa[s] = L[rowA[s] + (c ^ swA[s])];
+                for (int s = 0; s < TM; ++s) fa[s] = L[rowA[s] + (c ^ swA[s])];
 #pragma unroll
-            for (int t = 0; t < TN; ++t) fb[t] = L[rowB[t] + (c ^ swB[t])];
-#pragma unroll
-            for (int t = 0; t < TN; ++t)
-#pragma unroll
-                for (int s = 0; s < TM; ++s)
-                    acc[t][s] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fb[t], fa[s], acc[t][s], 0, 0, 0);
-            if constexpr (ACC16) {
-                // fp16 accumulation: the running sum is rounded to fp16 at
-                // the end of every aligned 32-deep group of k.
+                for (int t = 0; t < TN; ++t) fb[t] = L[rowB[t] + (c ^ swB[t])];
 #pragma unroll
                 for (int t = 0; t < TN; ++t)
 #pragma unroll
                     for (int s = 0; s < TM; ++s)
+                        acc[t][s] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fb[t], fa[s], acc[t][s], 0, 0, 0);
+                if constexpr (ACC16) {
+                    // fp16 accumulation: the running sum is rounded to fp16 at
+                    // the end of every aligned 32-deep group of k.
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) acc[t][s][e] = (float)(_Float16)acc[t][s][e];
+                    for (int t = 0; t < TN; ++t)
+#pragma unroll
+                        for (int s = 0; s < TM; ++s)
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) acc[t][s][e] = (float)(_Float16)acc[t][s][e];
+                }
             }
+            if (more) {
+                ca.store(&lds[cur ^ 1][0], tid);
+                cb.store(&lds[cur ^ 1][BM * KCH], tid);
+            }
+            __syncthreads();
         }
-        if (more) {
-            ca.store(&lds[cur ^ 1][0], tid);
-            cb.store(&lds[cur ^ 1][BM * KCH], tid);
-        }
-        __syncthreads();
+        if (seg == 1 && p.sub) negate_acc();
     }
 
-    // Epilogue on registers: + bias, ReLU, fp16, one 16-byte store per lane
-    // per pair of MFMA blocks.
+    // Epilogue on registers: +/- bias, activation, fp16, one 16-byte store
+    // per lane per pair of MFMA blocks.
 #pragma unroll
     for (int pr = 0; pr < TN / 2; ++pr) {
         const int j = n0 + wn * WTN + 32 * pr + 8 * kq;
         float b[8];
-        if (p.bias != nullptr) {
+        if (p.bias_kind == BIAS_ROW) {
             h8 bv = zero_h8();
             if (j < p.N) bv = load8<VEC>(p.bias + j, p.N - j);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) b[e] = (float)bv[e];
+            for (int e = 0; e < 8; ++e) b[e] = p.bias_sign * (float)bv[e];
         } else {
 #pragma unroll
             for (int e = 0; e < 8; ++e) b[e] = 0.f;
@@ -269,13 +297,19 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_generic(GemmArgs p
 #pragma unroll
         for (int s = 0; s < TM; ++s) {
             const int i = m0 + wm * WTM + 16 * s + (lane & 15);
+            float x[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[e] = (e < 4 ? acc[2 * pr][s][e] : acc[2 * pr + 1][s][e - 4]) + b[e];
+            if (p.bias_kind == BIAS_FULL) {
+                h8 bv = zero_h8();
+                if (i < p.M && j < p.N) bv = load8<VEC>(p.bias + (int64_t)i * p.ldbias + j, p.N - j);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[e] += p.bias_sign * (float)bv[e];
+            }
+            activate(p.act, x);
             h8 o;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                float x = (e < 4 ? acc[2 * pr][s][e] : acc[2 * pr + 1][s][e - 4]) + b[e];
-                if (p.relu) x = x > 0.f ? x : 0.f;
-                o[e] = (_Float16)x;
-            }
+            for (int e = 0; e < 8; ++e) o[e] = (_Float16)x[e];
             if (i < p.M && j < p.N) {
                 _Float16 *dst = p.C + (int64_t)i * p.ldc + j;
                 if (VEC && j + 8 <= p.N) {

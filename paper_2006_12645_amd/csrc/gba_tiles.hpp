@@ -54,44 +54,46 @@ constexpr TileCfg GENERIC_TILE = {64, 64, 2, 2, 1, 2};
 
 typedef hipError_t (*LaunchFn)(const GemmArgs &, hipStream_t);
 
-// Per operand-layout pair: fast[tile][acc16] for the aligned fast path
-// (null for fp16 accumulation with split-K), generic[acc16] otherwise.
+// Per operand-layout pair and kernel variant: fast[tile][acc16] for the
+// aligned fast path (null for fp16 accumulation with split-K),
+// generic[acc16] otherwise.
 struct LayoutTable {
     LaunchFn fast[NUM_TILES][2];
     LaunchFn generic[2];
 };
 
-template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16>
+template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool PRO, bool DUAL>
 hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
 {
     dim3 grid((unsigned)(a.tiles_m * a.tiles_n)), block(64 * WM * WN * SK);
-    hipLaunchKernelGGL((gemm_bias_act_fast<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, true>), grid, block,
-                       0, s, a);
-    return hipGetLastError();
-}
-
-// Launch-table entry for fp16 accumulation: none with split-K.
-template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB>
-constexpr LaunchFn fast_acc16()
-{
-    if constexpr (SK == 1) return &launch_fast<BM, BN, WM, WN, SK, NSTG, LA, LB, true>;
-    else return nullptr;
-}
-
-template <int LA, int LB, bool ACC16>
-hipError_t launch_generic(const GemmArgs &a, hipStream_t s)
-{
-    constexpr TileCfg c = GENERIC_TILE;
-    dim3 grid((unsigned)(a.tiles_m * a.tiles_n)), block(64 * c.wm * c.wn);
-    hipLaunchKernelGGL((gemm_bias_act_generic<c.bm, c.bn, c.wm, c.wn, LA, LB, ACC16, false>), grid,
+    hipLaunchKernelGGL((gemm_bias_act_fast<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, true, PRO, DUAL>), grid,
                        block, 0, s, a);
     return hipGetLastError();
 }
 
-// Host-side launch tables, one per layout pair (defined in gba_gemm_<layout>.hip).
-const LayoutTable &table_RR();
-const LayoutTable &table_RC();
-const LayoutTable &table_CR();
-const LayoutTable &table_CC();
+// Launch-table entry for fp16 accumulation: none with split-K.
+template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool PRO, bool DUAL>
+constexpr LaunchFn fast_acc16()
+{
+    if constexpr (SK == 1) return &launch_fast<BM, BN, WM, WN, SK, NSTG, LA, LB, true, PRO, DUAL>;
+    else return nullptr;
+}
+
+template <int LA, int LB, bool ACC16, bool PRO, bool DUAL>
+hipError_t launch_generic(const GemmArgs &a, hipStream_t s)
+{
+    constexpr TileCfg c = GENERIC_TILE;
+    dim3 grid((unsigned)(a.tiles_m * a.tiles_n)), block(64 * c.wm * c.wn);
+    hipLaunchKernelGGL((gemm_bias_act_generic<c.bm, c.bn, c.wm, c.wn, LA, LB, ACC16, false, PRO, DUAL>),
+                       grid, block, 0, s, a);
+    return hipGetLastError();
+}
+
+// Host-side launch table of one layout pair (LA, LB) and variant: PRO = ReLU
+// prologue on the left operands, DUAL = a second product.  Each
+// specialisation is defined in its own instantiation unit
+// (gba_gemm_unit.hip compiled once per combination).
+template <int LA, int LB, bool PRO, bool DUAL>
+const LayoutTable &layout_table();
 
 }  // namespace gba

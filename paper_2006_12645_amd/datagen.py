@@ -89,7 +89,24 @@ WORKLOADS = {
                                        ("f32", "f16"), 520),
     "ragged1000": Workload("ragged1000", 1000, 1000, 1000, ("RR", "RC", "CR", "CC"), "uniform",
                            ("f32", "f16"), 530),
+    # the other idioms at the headline shape: relu(A).B + bias -> ReLU
+    # (prologue), and A.B + P.Q + bias -> ReLU with K2 = K (sum of matmuls)
+    "prologue4096_RC": Workload("prologue4096_RC", 4096, 4096, 4096, ("RC",), "uniform", ("f32",),
+                                600, {"prologue": "relu"}),
+    "sum4096_RC": Workload("sum4096_RC", 4096, 4096, 4096, ("RC",), "uniform", ("f32",), 610,
+                           {"second": "add", "K2": 4096}),
 }
+
+
+def second_inputs(w: Workload):
+    """Logical P (M x K2) and Q (K2 x N) of a sum-of-matmuls workload,
+    drawn like A and B."""
+    K2 = w.extra["K2"]
+    s = w.seed_base + 10
+    if w.dist == "uniform":
+        return uniform_f16(s + 1, (w.M, K2)), uniform_f16(s + 2, (K2, w.N))
+    std = 1.0 / np.sqrt(K2)
+    return normal_f16(s + 1, (w.M, K2), std), normal_f16(s + 2, (K2, w.N), std)
 
 
 def logical_inputs(w: Workload):
@@ -110,7 +127,13 @@ def logical_inputs(w: Workload):
 
 
 def random_problem(seed: int, M: int, N: int, K: int, dist: str = "uniform"):
-    """Logical A, B, bias for an arbitrary shape (uniform[-1,1] or integer data)."""
+    """Logical A, B, bias for an arbitrary shape: uniform[-1,1], integer
+    ({-1,0,1} operands, bias in -8..8) or mlp (N(0, 1/sqrt(K)), bias
+    N(0, 0.1)) data."""
+    if dist == "mlp":
+        std = 1.0 / np.sqrt(max(K, 1))
+        return (normal_f16(seed + 1, (M, K), std), normal_f16(seed + 2, (K, N), std),
+                normal_f16(seed + 3, (N,), 0.1))
     if dist == "uniform":
         return (uniform_f16(seed + 1, (M, K)), uniform_f16(seed + 2, (K, N)),
                 uniform_f16(seed + 3, (N,)))

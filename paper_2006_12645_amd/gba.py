@@ -13,15 +13,33 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libgba.so")
 
 GBA_ROW_MAJOR, GBA_COL_MAJOR = 0, 1
-GBA_ACT_NONE, GBA_ACT_RELU = 0, 1
+GBA_ACT_NONE, GBA_ACT_RELU, GBA_ACT_SIGMOID, GBA_ACT_TANH = 0, 1, 2, 3
 GBA_ACC_F32, GBA_ACC_F16 = 0, 1
 GBA_OK, GBA_EINVAL, GBA_EUNSUPPORTED, GBA_EHIP = 0, 1, 2, 3
+GBA_PRO_NONE, GBA_PRO_RELU = 0, 1
+GBA_SECOND_NONE, GBA_SECOND_ADD, GBA_SECOND_SUB = 0, 1, 2
+GBA_BIAS_NONE, GBA_BIAS_ROW, GBA_BIAS_FULL = 0, 1, 2
+GBA_OP_ADD, GBA_OP_SUB = 0, 1
 
-ACTS = {"none": GBA_ACT_NONE, "relu": GBA_ACT_RELU}
+ACTS = {"none": GBA_ACT_NONE, "relu": GBA_ACT_RELU, "sigmoid": GBA_ACT_SIGMOID,
+        "tanh": GBA_ACT_TANH}
 ACCS = {"f32": GBA_ACC_F32, "fp32": GBA_ACC_F32, "f16": GBA_ACC_F16, "fp16": GBA_ACC_F16}
+OPS = {"add": GBA_OP_ADD, "sub": GBA_OP_SUB}
+
+_i64, _int, _vp, _cp = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_char_p
+
+
+class FusedDesc(ctypes.Structure):
+    """Mirror of struct gba_fused_desc (C enums are int)."""
+    _fields_ = [("layoutA", _int), ("layoutB", _int), ("M", _i64), ("N", _i64), ("K", _i64),
+                ("A", _vp), ("lda", _i64), ("B", _vp), ("ldb", _i64),
+                ("prologue", _int), ("second", _int), ("K2", _i64),
+                ("P", _vp), ("ldp", _i64), ("Q", _vp), ("ldq", _i64),
+                ("bias_kind", _int), ("bias_op", _int), ("bias", _vp), ("ldbias", _i64),
+                ("act", _int), ("accum", _int), ("C", _vp), ("ldc", _i64), ("tile_id", _int)]
+
 
 # Every function include/gba.h declares, with its ctypes signature.
-_i64, _int, _vp, _cp = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_char_p
 _GEMM_ARGS = [_int, _int, _i64, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _vp, _i64, _int, _int]
 SIGNATURES = {
     "gemm_bias_act": (_int, _GEMM_ARGS + [_vp]),
@@ -31,6 +49,9 @@ SIGNATURES = {
     "gba_select_tile": (_int, [_int, _int, _i64, _i64, _i64, _int]),
     "gba_bias_add_f16": (_int, [_i64, _i64, _vp, _i64, _vp, _vp]),
     "gba_relu_f16": (_int, [_i64, _i64, _vp, _i64, _vp]),
+    "gba_add_f16": (_int, [_i64, _i64, _vp, _i64, _vp, _i64, _vp]),
+    "gba_fused_desc_init": (None, [ctypes.POINTER(FusedDesc)]),
+    "gba_fused_gemm": (_int, [ctypes.POINTER(FusedDesc), _vp]),
     "gba_status_string": (_cp, [_int]),
     "gba_version": (_cp, []),
 }
@@ -72,15 +93,18 @@ def _stream_handle(stream, device):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
-def operand_layout(t, rows, cols):
-    """(layout, ld) of a 2-D tensor holding a logical rows x cols matrix."""
+def operand_layout(t, rows, cols, want=None):
+    """(layout, ld) of a 2-D tensor holding a logical rows x cols matrix;
+    ``want`` asks for that layout (for operands that must match another)."""
     if t.dim() != 2 or tuple(t.shape) != (rows, cols):
         raise ValueError(f"expected a {rows}x{cols} matrix, got shape {tuple(t.shape)}")
     s0, s1 = t.stride()
-    if (s1 == 1 or cols <= 1) and (rows <= 1 or s0 >= cols):
+    if want in (None, GBA_ROW_MAJOR) and (s1 == 1 or cols <= 1) and (rows <= 1 or s0 >= cols):
         return GBA_ROW_MAJOR, (s0 if rows > 1 else max(cols, 1))
-    if (s0 == 1 or rows <= 1) and (cols <= 1 or s1 >= rows):
+    if want in (None, GBA_COL_MAJOR) and (s0 == 1 or rows <= 1) and (cols <= 1 or s1 >= rows):
         return GBA_COL_MAJOR, (s1 if cols > 1 else max(rows, 1))
+    if want is not None:
+        raise ValueError("P and Q must be stored in the layouts of A and B")
     raise ValueError("operand must be row- or column-major (one unit stride)")
 
 
@@ -128,6 +152,90 @@ def gemm_bias_act(A, B, bias=None, act="relu", accum="f32", out=None, tile=None,
     return out
 
 
+def new_desc():
+    """A FusedDesc holding the library's defaults (gba_fused_desc_init)."""
+    d = FusedDesc()
+    lib().gba_fused_desc_init(ctypes.byref(d))
+    return d
+
+
+def fused_gemm_desc(desc, stream=None, device=None):
+    """Launch gba_fused_gemm on a filled FusedDesc (raises on error)."""
+    _check(lib().gba_fused_gemm(ctypes.byref(desc), _stream_handle(stream, device)), "gba_fused_gemm")
+
+
+def fused_gemm(A, B, *, P=None, Q=None, second="add", prologue=None, bias=None, bias_op="add",
+               act="relu", accum="f32", out=None, tile=None, stream=None):
+    """out = act((pro(A) @ B  +/-  pro(P) @ Q)  +/-  bias) in one kernel.
+
+    A (M, K), B (K, N): fp16 CUDA tensors, row- or column-major.  P (M, K2)
+    and Q (K2, N), if given, must use the layouts of A and B; ``second`` is
+    "add" or "sub".  prologue: None or "relu" (applied to A and P).  bias:
+    None, an (N,) vector or a row-major (M, N) matrix; ``bias_op`` "add" or
+    "sub".  act: "none", "relu", "sigmoid", "tanh".  out: (M, N) row-major
+    fp16, allocated when None.
+    """
+    import torch
+    M, K = A.shape
+    Kb, N = B.shape
+    if Kb != K:
+        raise ValueError("inner dimensions of A and B differ")
+    if (P is None) != (Q is None):
+        raise ValueError("P and Q come together")
+    for name, t in (("A", A), ("B", B), ("P", P), ("Q", Q), ("bias", bias), ("out", out)):
+        if t is not None and (t.dtype != torch.float16 or not t.is_cuda):
+            raise TypeError(f"{name} must be a float16 CUDA tensor")
+    d = new_desc()
+    d.M, d.N, d.K = M, N, K
+    d.A, d.B = A.data_ptr(), B.data_ptr()
+    d.prologue = {None: GBA_PRO_NONE, "none": GBA_PRO_NONE, "relu": GBA_PRO_RELU}[prologue]
+    K2 = 0
+    if P is not None:
+        Mp, K2 = P.shape
+        K2q, Nq = Q.shape
+        if Mp != M or Nq != N or K2q != K2:
+            raise ValueError("P @ Q must be an (M, N) product")
+        d.second = {"add": GBA_SECOND_ADD, "sub": GBA_SECOND_SUB}[second]
+        d.K2, d.P, d.Q = K2, P.data_ptr(), Q.data_ptr()
+    # Layouts come from the operands that are read; an empty reduction's
+    # operands are never read, so their layout and leading dimension are
+    # free (the smallest legal ones are passed).
+    if K > 0:
+        d.layoutA, d.lda = operand_layout(A, M, K)
+        d.layoutB, d.ldb = operand_layout(B, K, N)
+    if K2 > 0:
+        want_a, want_b = (d.layoutA, d.layoutB) if K > 0 else (None, None)
+        d.layoutA, d.ldp = operand_layout(P, M, K2, want=want_a)
+        d.layoutB, d.ldq = operand_layout(Q, K2, N, want=want_b)
+    row_a, row_b = d.layoutA == GBA_ROW_MAJOR, d.layoutB == GBA_ROW_MAJOR
+    if K == 0:
+        d.lda, d.ldb = (0 if row_a else M), (N if row_b else 0)
+    if P is not None and K2 == 0:
+        d.ldp, d.ldq = (0 if row_a else M), (N if row_b else 0)
+    if bias is not None:
+        if bias.dim() == 1:
+            if bias.shape[0] != N or (N > 1 and bias.stride(0) != 1):
+                raise ValueError("a vector bias must be a contiguous (N,) tensor")
+            d.bias_kind = GBA_BIAS_ROW
+        else:
+            if tuple(bias.shape) != (M, N):
+                raise ValueError("a matrix bias must be (M, N)")
+            d.bias_kind = GBA_BIAS_FULL
+            d.ldbias = _row_major_ld(bias, "bias")
+        d.bias = bias.data_ptr()
+        d.bias_op = OPS[bias_op]
+    d.act = ACTS[act]
+    d.accum = ACCS[accum]
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float16, device=A.device)
+    if out.dim() != 2 or tuple(out.shape) != (M, N):
+        raise ValueError("out must be an (M, N) matrix")
+    d.C, d.ldc = out.data_ptr(), _row_major_ld(out, "out")
+    d.tile_id = -1 if tile is None else int(tile)
+    fused_gemm_desc(d, stream, A.device)
+    return out
+
+
 def bias_add_(C, bias, stream=None):
     """In place: C = fp16(C + bias[None, :]) (unfused baseline piece)."""
     M, N = C.shape
@@ -143,6 +251,16 @@ def relu_(C, stream=None):
     ldc = _row_major_ld(C, "C")
     _check(lib().gba_relu_f16(M, N, C.data_ptr(), ldc, _stream_handle(stream, C.device)),
            "gba_relu_f16")
+    return C
+
+
+def add_(C, X, stream=None):
+    """In place: C = fp16(C + X) (unfused baseline piece)."""
+    M, N = C.shape
+    if tuple(X.shape) != (M, N):
+        raise ValueError("X must have the shape of C")
+    _check(lib().gba_add_f16(M, N, C.data_ptr(), _row_major_ld(C, "C"), X.data_ptr(),
+                             _row_major_ld(X, "X"), _stream_handle(stream, C.device)), "gba_add_f16")
     return C
 
 

@@ -149,3 +149,109 @@ def test_layout_inference_on_cpu_tensors():
     assert gba.operand_layout(a[:, :7], 6, 7) == (gba.GBA_ROW_MAJOR, 10)
     with pytest.raises(ValueError):
         gba.operand_layout(a[::2, ::2], 3, 5)
+
+
+def test_fused_desc_matches_c_layout(tmp_path):
+    """The ctypes mirror of struct gba_fused_desc has the C compiler's
+    size and field offsets."""
+    import subprocess
+    fields = [f[0] for f in gba.FusedDesc._fields_]
+    prog = tmp_path / "desc.c"
+    prog.write_text("#include <stdio.h>\n#include <stddef.h>\n#include \"gba.h\"\nint main(void){\n"
+                    "printf(\"%zu\\n\", sizeof(gba_fused_desc));\n" +
+                    "".join(f"printf(\"%zu\\n\", offsetof(gba_fused_desc, {f}));\n" for f in fields) +
+                    "return 0;}\n")
+    exe = tmp_path / "desc"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), "-o", str(exe), str(prog)],
+                   check=True)
+    vals = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
+                                           check=True).stdout.split()]
+    assert vals[0] == ctypes.sizeof(gba.FusedDesc)
+    assert vals[1:] == [getattr(gba.FusedDesc, f).offset for f in fields]
+
+
+def test_fused_desc_defaults():
+    d = gba.new_desc()
+    assert (d.layoutA, d.layoutB, d.prologue, d.second, d.bias_kind, d.bias_op, d.act,
+            d.accum, d.tile_id) == (0, 0, 0, 0, 0, 0, 0, 0, -1)
+    assert d.A is None and d.C is None and d.M == 0 and d.K2 == 0
+    gba.lib().gba_fused_desc_init(None)  # ignored, no crash
+
+
+def fused(**kw):
+    """gba_fused_gemm on a valid 64^3 request with two products, a full
+    bias and ReLU, modified by kw (pointers are never dereferenced: every
+    case is rejected or empty before any launch)."""
+    d = gba.new_desc()
+    d.layoutA, d.layoutB, d.M, d.N, d.K = 0, 1, 64, 64, 64
+    d.A, d.lda, d.B, d.ldb = FAKE, 64, FAKE, 64
+    d.second, d.K2, d.P, d.ldp, d.Q, d.ldq = gba.GBA_SECOND_ADD, 32, FAKE, 32, FAKE, 32
+    d.bias_kind, d.bias, d.ldbias = gba.GBA_BIAS_FULL, FAKE, 64
+    d.act, d.C, d.ldc = gba.GBA_ACT_RELU, FAKE, 64
+    for k, v in kw.items():
+        setattr(d, k, v)
+    return gba.lib().gba_fused_gemm(ctypes.byref(d), None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(prologue=2), gba.GBA_EINVAL),
+    (dict(second=3), gba.GBA_EINVAL),
+    (dict(second=-1), gba.GBA_EINVAL),
+    (dict(bias_kind=3), gba.GBA_EINVAL),
+    (dict(bias_op=2), gba.GBA_EINVAL),
+    (dict(act=4), gba.GBA_EINVAL),
+    (dict(act=-1), gba.GBA_EINVAL),
+    (dict(accum=2), gba.GBA_EINVAL),
+    (dict(tile_id=16), gba.GBA_EINVAL),
+    (dict(K2=-1), gba.GBA_EINVAL),
+    (dict(ldp=31), gba.GBA_EINVAL),
+    (dict(layoutA=1, ldp=63), gba.GBA_EINVAL),
+    (dict(ldq=31), gba.GBA_EINVAL),
+    (dict(layoutB=0, ldq=63), gba.GBA_EINVAL),
+    (dict(P=None), gba.GBA_EINVAL),
+    (dict(Q=None), gba.GBA_EINVAL),
+    (dict(bias=None), gba.GBA_EINVAL),
+    (dict(ldbias=63), gba.GBA_EINVAL),
+    (dict(ldbias=-1), gba.GBA_EINVAL),
+    (dict(C=None), gba.GBA_EINVAL),
+    (dict(A=None), gba.GBA_EINVAL),
+    (dict(P=FAKE + 1), gba.GBA_EUNSUPPORTED),
+    (dict(Q=FAKE + 1), gba.GBA_EUNSUPPORTED),
+    (dict(K2=2**31, ldp=2**31), gba.GBA_EUNSUPPORTED),
+    # with no second product, P/Q/K2 are not read; a row bias ignores ldbias
+    (dict(second=0, P=None, Q=None, K2=-7, ldp=-1, M=0), gba.GBA_OK),
+    (dict(bias_kind=gba.GBA_BIAS_ROW, ldbias=-3, N=0), gba.GBA_OK),
+    (dict(M=0, A=None, B=None, P=None, Q=None, C=None, bias=None), gba.GBA_OK),
+])
+def test_fused_validation(kw, status):
+    assert fused(**kw) == status
+
+
+def test_fused_validation_null_desc():
+    assert gba.lib().gba_fused_gemm(None, None) == gba.GBA_EINVAL
+
+
+def test_generalised_act_enum_accepted_by_gemm_bias_act():
+    # sigmoid and tanh pass validation (an empty problem launches nothing)
+    assert gemm(M=0, act=gba.GBA_ACT_SIGMOID) == gba.GBA_OK
+    assert gemm(M=0, act=gba.GBA_ACT_TANH) == gba.GBA_OK
+    assert gemm(act=4) == gba.GBA_EINVAL
+
+
+def test_operand_layout_with_required_layout():
+    import torch
+    p = torch.zeros(1, 9, dtype=torch.float16)
+    assert gba.operand_layout(p, 1, 9, want=gba.GBA_COL_MAJOR) == (gba.GBA_COL_MAJOR, 1)
+    assert gba.operand_layout(p, 1, 9, want=gba.GBA_ROW_MAJOR) == (gba.GBA_ROW_MAJOR, 9)
+    q = torch.zeros(6, 10, dtype=torch.float16)
+    with pytest.raises(ValueError):
+        gba.operand_layout(q, 6, 10, want=gba.GBA_COL_MAJOR)
+
+
+def test_add_validation():
+    L = gba.lib()
+    assert L.gba_add_f16(-1, 4, FAKE, 4, FAKE, 4, None) == gba.GBA_EINVAL
+    assert L.gba_add_f16(4, 4, FAKE, 4, None, 4, None) == gba.GBA_EINVAL
+    assert L.gba_add_f16(4, 4, FAKE, 4, FAKE, 3, None) == gba.GBA_EINVAL
+    assert L.gba_add_f16(4, 4, FAKE, 4, FAKE + 1, 4, None) == gba.GBA_EUNSUPPORTED
+    assert L.gba_add_f16(0, 4, None, 4, None, 4, None) == gba.GBA_OK

@@ -1,0 +1,311 @@
+"""HIP path vs the CPU oracle for the wider idioms of gba_fused_gemm: ReLU
+prologue (Listing 4), sum / difference of two products (Listing 5), full or
+subtracted bias, Sigmoid and Tanh -- element by element, through the C ABI.
+
+Each case prints its name before touching the GPU.  Inputs come from the
+seeded generators in paper_2006_12645_amd.datagen; expected values from
+the oracle only.
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2006_12645_amd import datagen as D
+from paper_2006_12645_amd import gba
+
+import gpu_util as U
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+LAYOUTS = ["RR", "RC", "CR", "CC"]
+NUM_TILES = 16
+ACT = {"none": O.ACT_NONE, "relu": O.ACT_RELU, "sigmoid": O.ACT_SIGMOID, "tanh": O.ACT_TANH}
+
+
+def announce(*what):
+    print("CASE", *what, flush=True)
+
+
+@pytest.fixture(autouse=True, scope="module")
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    gba.lib()
+    yield
+
+
+class Problem:
+    """Logical operands of one fused request and its oracle."""
+
+    def __init__(self, seed, M, N, K, K2=None, dist="uniform", bias="row", full_bias=False):
+        self.M, self.N, self.K, self.K2 = M, N, K, K2
+        self.A, self.B, row = D.random_problem(seed, M, N, K, dist)
+        self.P = self.Q = None
+        if K2 is not None:
+            self.P, self.Q, _ = D.random_problem(seed + 50, M, N, K2, dist)
+        if bias is None:
+            self.bias = None
+        elif full_bias:
+            lo, hi = (-8, 8) if dist == "int" else (-1, 1)
+            self.bias = (D.integer_f16(seed + 60, (M, N), lo, hi) if dist == "int"
+                         else D.uniform_f16(seed + 60, (M, N), lo, hi))
+        else:
+            self.bias = row
+
+    def oracle(self, prologue=False, second="add", bias_op="add", act="relu", rows=None):
+        sec = 0 if self.P is None else (1 if second == "add" else -1)
+        return O.fused(D.store(self.A, D.ROW), D.ROW, D.store(self.B, D.COL), D.COL,
+                       self.M, self.N, self.K, prologue_relu=prologue, second=sec,
+                       p_store=None if self.P is None else D.store(self.P, D.ROW),
+                       q_store=None if self.Q is None else D.store(self.Q, D.COL),
+                       K2=self.K2 or 0, bias=self.bias, bias_sign=1 if bias_op == "add" else -1,
+                       act=ACT[act], rows=rows)
+
+    def gpu(self, layout, prologue=False, second="add", bias_op="add", act="relu", accum="f32",
+            tile=None, pad=0, offset=False):
+        la, lb = D.LAYOUT_NAMES[layout]
+
+        def dev(x, lay):
+            if x is None:
+                return None
+            if not offset:
+                return U.device_operand(x, lay, pad)
+            # storage shifted by one element: 2-byte aligned only (general path)
+            rows, cols = x.shape
+            ext = (cols if lay == D.ROW else rows) + pad
+            st = D.store(x, lay, ext)
+            flat = torch.empty(st.size + 1, dtype=torch.float16, device="cuda")
+            t = flat[1:].view(st.shape)
+            t.copy_(torch.from_numpy(st).cuda())
+            return t[:, :cols] if lay == D.ROW else t[:, :rows].t()
+
+        dbias = None
+        if self.bias is not None:
+            dbias = (torch.from_numpy(self.bias).cuda() if self.bias.ndim == 1
+                     else dev(self.bias, D.ROW))
+        o = gba.fused_gemm(dev(self.A, la), dev(self.B, lb), P=dev(self.P, la), Q=dev(self.Q, lb),
+                           second=second, prologue="relu" if prologue else None, bias=dbias,
+                           bias_op=bias_op, act=act, accum=accum, tile=tile)
+        torch.cuda.synchronize()
+        return o.cpu().numpy()
+
+
+# ----------------------------------------------------------------------------
+# Each idiom in all layouts, several tiles plus a ragged tail on the fast path
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_prologue_relu(layout):
+    announce("prologue_relu", layout)
+    pr = Problem(700, 520, 392, 264)
+    U.assert_close(pr.gpu(layout, prologue=True), pr.oracle(prologue=True), what=f"prologue {layout}")
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("second", ["add", "sub"])
+def test_sum_of_products(layout, second):
+    announce("sum_of_products", layout, second)
+    pr = Problem(710, 520, 392, 264, K2=136)
+    U.assert_close(pr.gpu(layout, second=second), pr.oracle(second=second),
+                   what=f"second {second} {layout}")
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("bias_op", ["add", "sub"])
+def test_full_bias(layout, bias_op):
+    announce("full_bias", layout, bias_op)
+    pr = Problem(720, 264, 392, 200, full_bias=True)
+    U.assert_close(pr.gpu(layout, bias_op=bias_op, act="none", pad=8),
+                   pr.oracle(bias_op=bias_op, act="none"), what=f"full bias {bias_op} {layout}")
+
+
+@pytest.mark.parametrize("layout", ["RC", "CR"])
+@pytest.mark.parametrize("act", ["sigmoid", "tanh", "none", "relu"])
+def test_activations(layout, act):
+    announce("activation", layout, act)
+    pr = Problem(730, 328, 264, 512, dist="mlp")
+    got = pr.gpu(layout, act=act, bias_op="sub")
+    ref = pr.oracle(act=act, bias_op="sub")
+    U.assert_close(got, ref, what=f"{act} {layout}")
+    if act in ("sigmoid", "tanh"):
+        # bounded outputs: the error is the fp16 rounding plus a few fp32 ulps
+        err = np.abs(got.astype(np.float64) - ref)
+        assert err.max() <= 2e-3, err.max()
+
+
+def test_tanh_small_arguments():
+    """Pre-activations spread over [-2^-3, 2^-3]: both sides of the Taylor /
+    exponential switch of tanh, against the oracle to fp16 rounding."""
+    announce("tanh_small")
+    M, N, K = 256, 256, 64
+    A = D.uniform_f16(740, (M, K), -1, 1)
+    B = D.uniform_f16(741, (K, N), -1 / 64, 1 / 64)
+    pr = Problem(742, M, N, K, bias=None)
+    pr.A, pr.B = A, B
+    got = pr.gpu("RC", act="tanh").astype(np.float64)
+    ref = pr.oracle(act="tanh")
+    assert np.abs(ref).max() < 0.3 and (np.abs(ref) < 1 / 16).any() and (np.abs(ref) > 1 / 16).any()
+    assert (np.abs(got - ref) <= 1e-5 + 2.0 ** -10 * np.abs(ref)).all()
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_everything_at_once(layout):
+    announce("all_features", layout)
+    pr = Problem(750, 392, 520, 200, K2=328, full_bias=True)
+    kw = dict(prologue=True, second="sub", bias_op="sub", act="tanh")
+    U.assert_close(pr.gpu(layout, **kw, pad=16), pr.oracle(**kw), what=f"all {layout}")
+
+
+# ----------------------------------------------------------------------------
+# Every tile, and fp16 accumulation
+
+@pytest.mark.parametrize("tile", range(NUM_TILES))
+def test_every_tile_all_features(tile):
+    announce("tile", tile)
+    pr = Problem(760, 520, 392, 264, K2=200, full_bias=True)
+    kw = dict(prologue=True, second="sub", bias_op="add", act="relu")
+    U.assert_close(pr.gpu("RC", **kw, tile=tile), pr.oracle(**kw), what=f"tile {tile}")
+
+
+@pytest.mark.parametrize("tile", [1, 4, 6, 9])
+@pytest.mark.parametrize("layout", ["RC", "CR"])
+def test_fp16_accumulation_two_products(tile, layout):
+    announce("f16acc", tile, layout)
+    pr = Problem(770, 264, 392, 256, K2=128)
+    kw = dict(prologue=True, second="add", act="relu")
+    U.assert_close(pr.gpu(layout, **kw, accum="f16", tile=tile), pr.oracle(**kw), accum="f16",
+                   what=f"f16 tile {tile} {layout}")
+
+
+# ----------------------------------------------------------------------------
+# Integer data: every partial sum is a small integer, so results are exact
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("accum", ["f32", "f16"])
+@pytest.mark.parametrize("second", ["add", "sub"])
+def test_integer_exact(layout, accum, second):
+    announce("integer", layout, accum, second)
+    pr = Problem(780, 264, 328, 392, K2=136, dist="int", full_bias=True)
+    for kw in (dict(prologue=True, second=second, bias_op="sub", act="none"),
+               dict(prologue=False, second=second, bias_op="add", act="relu")):
+        got = pr.gpu(layout, accum=accum, **kw).astype(np.float64)
+        ref = pr.oracle(**kw)
+        assert np.array_equal(got, ref), (kw, np.abs(got - ref).max())
+
+
+@pytest.mark.parametrize("tile", [4, 10, 13, 14])
+def test_integer_exact_split_k(tile):
+    announce("integer_splitk", tile)
+    pr = Problem(790, 264, 392, 1000, K2=520, dist="int")
+    kw = dict(prologue=True, second="sub", act="none")
+    got = pr.gpu("RC", tile=tile, **kw).astype(np.float64)
+    assert np.array_equal(got, pr.oracle(**kw))
+
+
+# ----------------------------------------------------------------------------
+# Edge cases: empty reductions, small and ragged shapes, the general path
+
+@pytest.mark.parametrize("K,K2", [(0, 64), (64, 0), (0, 0), (8, 8), (1000, 24)])
+def test_empty_and_short_reductions(K, K2):
+    announce("short_reductions", K, K2)
+    pr = Problem(800, 264, 256, K, K2=K2)
+    kw = dict(prologue=True, second="sub", act="relu")
+    U.assert_close(pr.gpu("RC", **kw), pr.oracle(**kw), what=f"K={K} K2={K2}")
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 1, 1), (7, 13, 5, 9), (33, 65, 17, 3), (100, 36, 70, 130)])
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_general_path_sizes(shape, layout):
+    M, N, K, K2 = shape
+    announce("general_sizes", shape, layout)
+    pr = Problem(810, M, N, K, K2=K2, full_bias=True)
+    kw = dict(prologue=True, second="add", bias_op="sub", act="sigmoid")
+    U.assert_close(pr.gpu(layout, **kw), pr.oracle(**kw), what=f"{shape} {layout}")
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_unaligned_operands_general_path(layout):
+    announce("unaligned", layout)
+    pr = Problem(820, 200, 136, 72, K2=40, full_bias=True)
+    kw = dict(prologue=True, second="sub", bias_op="add", act="tanh")
+    U.assert_close(pr.gpu(layout, **kw, offset=True, pad=3), pr.oracle(**kw),
+                   what=f"unaligned {layout}")
+
+
+def test_gemm_bias_act_is_the_single_product_case():
+    """gemm_bias_act and gba_fused_gemm with one product and a row bias run
+    the same kernel: bitwise equal outputs."""
+    announce("single_product_equivalence")
+    pr = Problem(830, 520, 392, 264)
+    dA = U.device_operand(pr.A, D.ROW)
+    dB = U.device_operand(pr.B, D.COL)
+    dbias = torch.from_numpy(pr.bias).cuda()
+    a = gba.gemm_bias_act(dA, dB, dbias, act="relu")
+    b = gba.fused_gemm(dA, dB, bias=dbias, act="relu")
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_deterministic():
+    announce("deterministic")
+    pr = Problem(840, 520, 392, 264, K2=200, full_bias=True)
+    kw = dict(prologue=True, second="sub", act="tanh")
+    first = pr.gpu("RC", **kw)
+    for _ in range(2):
+        assert np.array_equal(pr.gpu("RC", **kw), first)
+
+
+def test_sum4096_sampled_rows():
+    """The sum-of-products workload at full size (4096^3 twice), checked on
+    sampled rows, in the launch the benchmark times."""
+    w = D.WORKLOADS["sum4096_RC"]
+    announce(w.name)
+    A, B, bias = D.logical_inputs(w)
+    P, Q = D.second_inputs(w)
+    rows = sorted({0, 1, 255, 256, 2047, 4095} | set(int(r) for r in
+                                                      np.random.default_rng(5).integers(0, w.M, 10)))
+    dA = U.device_operand(A, D.ROW)
+    dB = U.device_operand(B, D.COL)
+    dP = U.device_operand(P, D.ROW)
+    dQ = U.device_operand(Q, D.COL)
+    out = gba.fused_gemm(dA, dB, P=dP, Q=dQ, bias=torch.from_numpy(bias).cuda(), act="relu")
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()[rows]
+    ref = O.fused(D.store(A, D.ROW), D.ROW, D.store(B, D.COL), D.COL, w.M, w.N, w.K, second=1,
+                  p_store=D.store(P, D.ROW), q_store=D.store(Q, D.COL), K2=w.extra["K2"], bias=bias,
+                  act=O.ACT_RELU, rows=rows)
+    U.assert_close(got, ref, what=w.name)
+
+
+def test_prologue4096_sampled_rows():
+    w = D.WORKLOADS["prologue4096_RC"]
+    announce(w.name)
+    A, B, bias = D.logical_inputs(w)
+    rows = sorted({0, 255, 256, 4095} | set(int(r) for r in np.random.default_rng(6).integers(0, w.M, 10)))
+    out = gba.fused_gemm(U.device_operand(A, D.ROW), U.device_operand(B, D.COL), prologue="relu",
+                         bias=torch.from_numpy(bias).cuda(), act="relu")
+    torch.cuda.synchronize()
+    ref = O.fused(D.store(A, D.ROW), D.ROW, D.store(B, D.COL), D.COL, w.M, w.N, w.K,
+                  prologue_relu=True, bias=bias, act=O.ACT_RELU, rows=rows)
+    U.assert_close(out.cpu().numpy()[rows], ref, what=w.name)
+
+
+def test_unfused_add_piece():
+    """gba_add_f16 (the separate add of the unfused sum-of-matmuls chain):
+    the fp32 sum of two fp16 values is exact, so the result is that sum
+    rounded once to fp16 -- numpy's float16 addition."""
+    announce("unfused_add")
+    M, N = 77, 136
+    C = D.uniform_f16(850, (M, N), -4, 4)
+    X = D.uniform_f16(851, (M, N), -4, 4)
+    dC = U.device_operand(C, D.ROW, pad=8)
+    dX = U.device_operand(X, D.ROW, pad=0)
+    gba.add_(dC, dX)
+    torch.cuda.synchronize()
+    want = (C.astype(np.float32) + X.astype(np.float32)).astype(np.float16)
+    assert np.array_equal(dC.cpu().numpy(), want)
+    dC2 = U.device_operand(C, D.ROW)[:, 1:]      # 2-byte aligned view: scalar path
+    dX2 = U.device_operand(X, D.ROW)[:, 1:]
+    gba.add_(dC2, dX2)
+    torch.cuda.synchronize()
+    assert np.array_equal(dC2.cpu().numpy(), want[:, 1:])
