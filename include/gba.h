@@ -24,6 +24,8 @@
  *   - Arguments are validated on the host before anything is enqueued.  On
  *     any error nothing is launched and the output is left untouched.
  *   - Outputs must not alias inputs.
+ *   - Inputs are expected to be finite.  The outputs for NaN or infinite
+ *     inputs, and for results beyond the fp16 range, are not specified.
  */
 #ifndef GBA_H
 #define GBA_H

@@ -45,8 +45,18 @@ __device__ __forceinline__ h8 zero_h8()
     return z;
 }
 
-// max(x, 0) on eight fp16 values (the ReLU of a prologue).
-__device__ __forceinline__ h8 relu_h8(h8 v) { return __builtin_elementwise_max(v, zero_h8()); }
+typedef short s8 __attribute__((ext_vector_type(8)));
+
+// max(x, 0) on eight fp16 values (the ReLU of a prologue), as a signed
+// 16-bit integer max on the bit patterns: one v_pk_max_i16 per two values,
+// where a floating-point max would first canonicalise its inputs.  Every
+// finite fp16 with the sign bit set (and -0) becomes +0; positive values
+// are unchanged.
+__device__ __forceinline__ h8 relu_h8(h8 v)
+{
+    const s8 zero = {0, 0, 0, 0, 0, 0, 0, 0};
+    return __builtin_bit_cast(h8, __builtin_elementwise_max(__builtin_bit_cast(s8, v), zero));
+}
 
 // tanh from its odd Taylor series near 0 (|x| < 1/16, where the next term
 // is below 2^-28 relative) and from tanh|x| = (1 - e) / (1 + e),

@@ -322,7 +322,9 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
     constexpr int ROWB = BK * 2;              // bytes per LDS row
     constexpr int SUB = (BM + BN) * ROWB;     // bytes per k-group sub-stage
     constexpr int STAGE = SK * SUB;           // bytes per LDS stage
-    constexpr bool DEEP = DMA && LA == ROW && LB == COL;
+    constexpr bool DMA_A = DMA && LA == ROW;  // A copied straight into LDS
+    constexpr bool DMA_B = DMA && LB == COL;
+    constexpr bool DEEP = DMA_A && DMA_B;
     constexpr int NS = DEEP ? NSTG : 2;       // LDS stages
     static_assert((NS & (NS - 1)) == 0, "stage count must be a power of two");
     constexpr int PADN = BN + 4;              // fp32 row pitch of the split-K partial tiles
@@ -351,10 +353,9 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
     const int mc = m0 + BM <= p.M ? m0 : p.M - BM;
     const int nc = n0 + BN <= p.N ? n0 : p.N - BN;
 
-    constexpr bool DMA_A = DMA && LA == ROW;
     constexpr bool FRAG_RELU = PRO && DMA_A;  // ReLU on fragments (no register stage)
     using CopyA = std::conditional_t<DMA_A, DmaCopy<BM, NTG>, RegCopy<BM, NTG, LA == ROW, PRO>>;
-    using CopyB = std::conditional_t<DMA && LB == COL, DmaCopy<BN, NTG>, RegCopy<BN, NTG, LB == COL, false>>;
+    using CopyB = std::conditional_t<DMA_B, DmaCopy<BN, NTG>, RegCopy<BN, NTG, LB == COL, false>>;
     CopyA ca;
     CopyB cb;
 
