@@ -57,21 +57,42 @@ gba_status validate(const gba_fused_desc &d)
 
 bool tile_fits(int tile, int64_t M, int64_t N) { return M >= TILES[tile].bm && N >= TILES[tile].bn; }
 
-// Tile choice by problem shape (K is the total reduction length).  With
-// enough output tiles, the largest block tile that fits inside the problem
-// and still yields a workgroup for each of the 256 compute units.  With few
-// output tiles and a long reduction, intra-workgroup split-K over a small
-// tile (fp32 accumulation only): its four k-groups and four-stage copies
-// keep the memory system busy where the plain tiles would leave most
-// compute units idle.  Otherwise the tile with the most workgroups.
+// Tile choice by problem shape (K is the total reduction length), tuned on
+// MI355X over the workload shapes and random multiples of 128 (measured
+// sweeps of every tile, RC layout, fp32 accumulation):
+//   * the 256x256 tile (8 waves) as soon as it yields 136 workgroups: one
+//     round over 53% or more of the 256 compute units beats two rounds of
+//     a smaller tile;
+//   * else 128x128 (two workgroups per compute unit) from 260 workgroups,
+//     then 128x64 / 64x128 (the long side along the longer output side)
+//     from 400;
+//   * a long reduction (fp32 accumulation only) whose 64x64 tiles fit in
+//     one round of 88 to 256 workgroups takes 64x64 with two k-groups of
+//     waves (intra-workgroup split-K); with fewer output tiles still, 64x64
+//     with two k-groups while that makes more than 64 workgroups, else
+//     32x32 with four k-groups and four LDS stages;
+//   * else 64x64 from 200 workgroups, then 32x64, then 32x32.
+// The 256x128 and 128x256 tiles were never the fastest in those sweeps and
+// are only used when asked for.
 int select_tile(int64_t M, int64_t N, int64_t K, int accum)
 {
-    const int64_t CUS = 256;
-    static const int order[] = {1, 2, 3, 4, 5, 7, 6, 8, 9};
-    for (int t : order)
-        if (tile_fits(t, M, N) && ceil_div(M, TILES[t].bm) * ceil_div(N, TILES[t].bn) >= CUS) return t;
-    if (accum == GBA_ACC_F32 && K >= 4096 && tile_fits(13, M, N)) return 13;
-    for (int t : {6, 8, 9})
+    auto tiles = [&](int t) -> int64_t {
+        return tile_fits(t, M, N) ? ceil_div(M, TILES[t].bm) * ceil_div(N, TILES[t].bn) : 0;
+    };
+    if (tiles(1) >= 136) return 1;
+    if (tiles(4) >= 260) return 4;
+    const int t57 = N > M ? 7 : 5;
+    if (tiles(t57) >= 400) return t57;
+    if (accum == GBA_ACC_F32 && K >= 2048) {
+        const int64_t n11 = tiles(11), n8 = tiles(8);
+        if (n11 >= 88 && n11 <= 256) return 11;
+        if (n8 < 128 || (K >= 4096 && n8 <= 128)) {
+            if (n11 > 64) return 11;
+            if (tile_fits(13, M, N)) return 13;
+        }
+    }
+    if (tiles(6) >= 200) return 6;
+    for (int t : {8, 9})
         if (tile_fits(t, M, N)) return t;
     return -1;  // smaller than the smallest tile: general path
 }

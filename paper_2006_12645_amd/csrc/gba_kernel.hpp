@@ -204,15 +204,19 @@ __device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t rs, cha
 
 // Scheduling hints for one 16-deep slice of NM MFMAs: the NR fragment reads
 // for the next slice go first (so they have the whole slice to land), then
-// half of the MFMAs, then the CNT instructions of class MASK (staging writes
-// 0x200 or global copies 0x020), then the other half of the MFMAs.
-template <int NM, int NR, int MASK, int CNT>
+// the MFMAs, each followed by its share of the CNT instructions of class
+// MASK (staging writes 0x200 or global copies 0x020), so those are spread
+// evenly over the slice instead of queueing behind each other.
+template <int NM, int NR, int MASK, int CNT, int I = 0>
 __device__ __forceinline__ void sched_slice()
 {
-    __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, NM / 2, 0);
-    if constexpr (CNT > 0) __builtin_amdgcn_sched_group_barrier(MASK, CNT, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, NM - NM / 2, 0);
+    if constexpr (I == 0 && NR > 0) __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
+    if constexpr (I < NM) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        constexpr int c = (CNT * (I + 1)) / NM - (CNT * I) / NM;
+        if constexpr (CNT > 0 && c > 0) __builtin_amdgcn_sched_group_barrier(MASK, c, 0);
+        sched_slice<NM, NR, MASK, CNT, I + 1>();
+    }
 }
 
 // Register-staged copy of one operand tile (any layout): global -> registers
