@@ -29,6 +29,8 @@ def load_library(path):
     i64, vp = ctypes.c_int64, ctypes.c_void_p
     lib.oracle_f16_to_f64.restype = ctypes.c_double
     lib.oracle_f16_to_f64.argtypes = [ctypes.c_uint16]
+    lib.oracle_round_f16.restype = ctypes.c_double
+    lib.oracle_round_f16.argtypes = [ctypes.c_double]
     lib.oracle_gemm_bias_act_rows_f64.restype = ctypes.c_int
     lib.oracle_gemm_bias_act_rows_f64.argtypes = [
         ctypes.c_int, ctypes.c_int, i64, i64, i64, vp, i64, vp, i64, vp,
@@ -38,7 +40,7 @@ def load_library(path):
     lib.oracle_fused_rows_f64.argtypes = [
         ci, ci, i64, i64, i64, vp, i64, vp, i64,          # layouts, M N K, A lda, B ldb
         ci, ci, i64, vp, i64, vp, i64,                    # pro_relu, second, K2, P ldp, Q ldq
-        ci, ci, vp, i64, ci,                              # bias kind/sign, bias ldbias, act
+        ci, ci, vp, i64, ci, ci,                          # bias kind/sign, bias ldbias, act, acc16
         vp, i64, vp, i64, ci]                             # rows nrows, out ldo, nthreads
     return lib
 
@@ -112,6 +114,11 @@ def gemm_bias_act(a_store, layout_a, b_store, layout_b, M, N, K, bias=None,
     return out
 
 
+def round_f16(x: float, lib=None) -> float:
+    """The oracle's binary64 -> binary16 rounding (ties to even)."""
+    return (lib or _load()).oracle_round_f16(float(x))
+
+
 def _ld(store, default):
     return store.shape[1] if store is not None and store.ndim == 2 else default
 
@@ -119,13 +126,16 @@ def _ld(store, default):
 def fused(a_store, layout_a, b_store, layout_b, M, N, K, *, prologue_relu=False,
           second=0, p_store=None, q_store=None, K2=0, bias=None, bias_kind=None,
           bias_sign=1, act=ACT_RELU, lda=None, ldb=None, ldp=None, ldq=None, ldbias=None,
-          rows=None, nthreads=None, lib=None):
+          acc16=False, rows=None, nthreads=None, lib=None):
     """Oracle of the general fused operation as float64, shape (len(rows) or M, N).
 
     ``second`` is 0 (one product), +1 (add P.Q) or -1 (subtract P.Q); P and
     Q are stored like A and B.  ``bias`` is a length-N vector (bias_kind
     BIAS_ROW, the default for a 1-D bias) or an M x ldbias array (BIAS_FULL,
-    the default for a 2-D bias); ``bias_sign`` -1 subtracts it.
+    the default for a 2-D bias); ``bias_sign`` -1 subtracts it.  ``acc16``
+    evaluates the fp16-accumulation reading (running sum rounded to binary16
+    after every aligned group of 32 k of each product) instead of the exact
+    binary64 sums.
     """
     lib = lib or _load()
     a, b = _as_bits(a_store), _as_bits(b_store)
@@ -148,7 +158,7 @@ def fused(a_store, layout_a, b_store, layout_b, M, N, K, *, prologue_relu=False,
     rc = lib.oracle_fused_rows_f64(
         int(layout_a), int(layout_b), int(M), int(N), int(K), _ptr(a), int(lda), _ptr(b), int(ldb),
         int(bool(prologue_relu)), int(second), int(K2), _ptr(pp), int(ldp), _ptr(qq), int(ldq),
-        int(bias_kind), int(bias_sign), _ptr(bi), int(ldbias), int(act),
+        int(bias_kind), int(bias_sign), _ptr(bi), int(ldbias), int(act), int(bool(acc16)),
         _ptr(r), int(nrows), _ptr(out), int(max(N, 1)), int(nthreads or default_threads()))
     if rc != 0:
         raise ValueError(f"oracle rejected the arguments (rc={rc})")

@@ -56,6 +56,29 @@ double oracle_f16_to_f64(uint16_t h)
     return sign ? -v : v;
 }
 
+/*
+ * Round a binary64 value to the nearest binary16 value, ties to even
+ * (IEEE 754 roundTiesToEven), returned as a binary64.  Written from the
+ * format: a value in [2^(e-1), 2^e) has quantum 2^(e-11) in binary16; below
+ * 2^-14 (subnormals) the quantum is 2^-24.  Magnitudes of 65520 and above
+ * (halfway past the largest finite value 65504) become infinities.
+ */
+double oracle_round_f16(double x)
+{
+    if (isnan(x) || x == 0.0)
+        return x;
+    double ax = fabs(x);
+    if (ax >= 65520.0)
+        return copysign(INFINITY, x);
+    int e;
+    frexp(ax, &e);                       /* ax = m * 2^e, m in [0.5, 1) */
+    int q = e - 11;
+    if (q < -24)
+        q = -24;
+    double r = rint(ldexp(ax, -q));      /* exact scaling; rint rounds ties to even */
+    return copysign(ldexp(r, q), x);
+}
+
 typedef struct {
     int layout_a;
     int64_t M, N, K;
@@ -241,7 +264,7 @@ typedef struct {
     const uint16_t *A, *P;
     int64_t lda, ldp;
     const double *Bd, *Qd;    /* decoded logical B (K x N) and Q (K2 x N), row-major */
-    int pro_relu, second;
+    int pro_relu, second, acc16;
     int bias_kind, bias_sign;
     const uint16_t *bias;
     int64_t ldbias;
@@ -286,6 +309,28 @@ static void product_row(const fjob_t *J, const uint16_t *X, int64_t ldx, const d
     }
 }
 
+/*
+ * fp16 accumulation (the reading of the fp16-accumulation mode): one running
+ * sum per output, rounded to binary16 at the end of every aligned group of
+ * 32 reduction indices of a product (k = 32c .. 32c+31, the last group
+ * possibly partial); inside a group the products are summed exactly enough
+ * (binary64) that only the group-end rounding matters.  sign = +1 adds the
+ * product's terms, -1 subtracts them; s carries the running sum in and out.
+ */
+static void product_row_acc16(const fjob_t *J, const uint16_t *X, int64_t ldx, const double *Yd,
+                              int64_t K, int64_t i, double *s, double sign)
+{
+    for (int64_t k = 0; k < K; ++k) {
+        double x = sign * left_elem(J->layout_a, X, ldx, i, k, J->pro_relu);
+        const double *yrow = Yd + k * J->N;
+        for (int64_t j = 0; j < J->N; ++j)
+            s[j] = s[j] + x * yrow[j];
+        if (k % 32 == 31 || k == K - 1)
+            for (int64_t j = 0; j < J->N; ++j)
+                s[j] = oracle_round_f16(s[j]);
+    }
+}
+
 static void *fused_thread(void *arg)
 {
     fjob_t *J = (fjob_t *)arg;
@@ -299,12 +344,23 @@ static void *fused_thread(void *arg)
     }
     for (int64_t q = J->tid; q < J->nrows; q += J->nthreads) {
         int64_t i = J->rows ? J->rows[q] : q;
-        product_row(J, J->A, J->lda, J->Bd, J->K, i, c);
-        if (J->second != 0)
-            product_row(J, J->P, J->ldp, J->Qd, J->K2, i, r);
+        if (J->acc16) {
+            /* one running sum over both products; R is then already in c */
+            for (int64_t j = 0; j < J->N; ++j) {
+                c[j] = 0.0;
+                r[j] = 0.0;
+            }
+            product_row_acc16(J, J->A, J->lda, J->Bd, J->K, i, c, 1.0);
+            if (J->second != 0)
+                product_row_acc16(J, J->P, J->ldp, J->Qd, J->K2, i, c, J->second > 0 ? 1.0 : -1.0);
+        } else {
+            product_row(J, J->A, J->lda, J->Bd, J->K, i, c);
+            if (J->second != 0)
+                product_row(J, J->P, J->ldp, J->Qd, J->K2, i, r);
+        }
         double *o = J->out + q * J->ldo;
         for (int64_t j = 0; j < J->N; ++j) {
-            double z = J->second > 0 ? c[j] + r[j] : (J->second < 0 ? c[j] - r[j] : c[j]);
+            double z = J->acc16 ? c[j] : (J->second > 0 ? c[j] + r[j] : (J->second < 0 ? c[j] - r[j] : c[j]));
             double pre = z;
             if (J->bias_kind != OR_BIAS_NONE) {
                 double b = oracle_f16_to_f64(J->bias_kind == OR_BIAS_ROW ? J->bias[j]
@@ -332,15 +388,17 @@ static double *decode_right(int layout_b, int64_t K, int64_t N, const uint16_t *
 
 /*
  * second: 0 one product, +1 add R, -1 subtract R.  bias_sign: +1 add,
- * -1 subtract.  rows == NULL: every row (nrows must equal M).  Returns 0 on
- * success, 1 on bad arguments, 2 on allocation or thread failure.
+ * -1 subtract.  acc16: 0 binary64 sums (the definition), 1 the fp16
+ * accumulation described above product_row_acc16.  rows == NULL: every row
+ * (nrows must equal M).  Returns 0 on success, 1 on bad arguments, 2 on
+ * allocation or thread failure.
  */
 int oracle_fused_rows_f64(int layout_a, int layout_b, int64_t M, int64_t N, int64_t K,
                           const uint16_t *A, int64_t lda, const uint16_t *B, int64_t ldb,
                           int pro_relu, int second, int64_t K2, const uint16_t *P, int64_t ldp,
                           const uint16_t *Q, int64_t ldq, int bias_kind, int bias_sign,
-                          const uint16_t *bias, int64_t ldbias, int act, const int64_t *rows,
-                          int64_t nrows, double *out, int64_t ldo, int nthreads)
+                          const uint16_t *bias, int64_t ldbias, int act, int acc16,
+                          const int64_t *rows, int64_t nrows, double *out, int64_t ldo, int nthreads)
 {
     if (M < 0 || N < 0 || K < 0 || nrows < 0 || ldo < N)
         return 1;
@@ -348,7 +406,7 @@ int oracle_fused_rows_f64(int layout_a, int layout_b, int64_t M, int64_t N, int6
         return 1;
     if (act < OR_ACT_NONE || act > OR_ACT_TANH || bias_kind < OR_BIAS_NONE || bias_kind > OR_BIAS_FULL)
         return 1;
-    if (second < -1 || second > 1 || (bias_sign != 1 && bias_sign != -1))
+    if (second < -1 || second > 1 || (bias_sign != 1 && bias_sign != -1) || (acc16 != 0 && acc16 != 1))
         return 1;
     if ((bias_kind != OR_BIAS_NONE && !bias) || (bias_kind == OR_BIAS_FULL && ldbias < N))
         return 1;
@@ -388,7 +446,7 @@ int oracle_fused_rows_f64(int layout_a, int layout_b, int64_t M, int64_t N, int6
         goto done;
     }
     for (int t = 0; t < nthreads; ++t) {
-        fjob_t J = {layout_a, N, K, K2, A, P, lda, ldp, Bd, Qd, pro_relu, second, bias_kind,
+        fjob_t J = {layout_a, N, K, K2, A, P, lda, ldp, Bd, Qd, pro_relu, second, acc16, bias_kind,
                     bias_sign, bias, ldbias, act, rows, nrows, out, ldo, nthreads, t};
         jobs[t] = J;
     }

@@ -53,14 +53,14 @@ class Problem:
         else:
             self.bias = row
 
-    def oracle(self, prologue=False, second="add", bias_op="add", act="relu", rows=None):
+    def oracle(self, prologue=False, second="add", bias_op="add", act="relu", rows=None, acc16=False):
         sec = 0 if self.P is None else (1 if second == "add" else -1)
         return O.fused(D.store(self.A, D.ROW), D.ROW, D.store(self.B, D.COL), D.COL,
                        self.M, self.N, self.K, prologue_relu=prologue, second=sec,
                        p_store=None if self.P is None else D.store(self.P, D.ROW),
                        q_store=None if self.Q is None else D.store(self.Q, D.COL),
                        K2=self.K2 or 0, bias=self.bias, bias_sign=1 if bias_op == "add" else -1,
-                       act=ACT[act], rows=rows)
+                       act=ACT[act], rows=rows, acc16=acc16)
 
     def gpu(self, layout, prologue=False, second="add", bias_op="add", act="relu", accum="f32",
             tile=None, pad=0, offset=False):
@@ -175,6 +175,33 @@ def test_fp16_accumulation_two_products(tile, layout):
     kw = dict(prologue=True, second="add", act="relu")
     U.assert_close(pr.gpu(layout, **kw, accum="f16", tile=tile), pr.oracle(**kw), accum="f16",
                    what=f"f16 tile {tile} {layout}")
+
+
+def ulp16(x):
+    """Spacing of binary16 values at magnitude |x| (subnormal spacing below
+    2^-14)."""
+    e = np.floor(np.log2(np.maximum(np.abs(x), 2.0 ** -14)))
+    return 2.0 ** (e - 10)
+
+
+@pytest.mark.parametrize("tile", [1, 4, 6, 9, None])
+@pytest.mark.parametrize("layout", ["RC", "CR", "RR", "CC"])
+def test_fp16_accumulation_matches_its_emulation(tile, layout):
+    """fp16 accumulation against the oracle's emulation of the reading (the
+    running sum rounded to binary16 after every aligned group of 32 k).  The
+    GPU sums each group in fp32 in the MFMA's own order, so a group-end
+    rounding can land on the other side of a tie: allow one binary16 step of
+    the running sum, and require almost every output to agree to the output
+    rounding alone."""
+    announce("f16acc_emulation", tile, layout)
+    pr = Problem(860, 264, 328, 1000, K2=200, bias="row")
+    kw = dict(prologue=True, second="sub", act="none")
+    got = pr.gpu(layout, accum="f16", tile=tile, **kw).astype(np.float64)
+    emu = pr.oracle(acc16=True, **kw)
+    err = np.abs(got - emu)
+    assert (err <= 2 * ulp16(np.maximum(np.abs(emu), 64.0))).all(), err.max()
+    close = err <= 0.5 * ulp16(emu) + 1e-12
+    assert close.mean() >= 0.99, close.mean()
 
 
 # ----------------------------------------------------------------------------

@@ -10,6 +10,7 @@ from oracle import build_oracle
 from oracle import oracle as O
 import oracle_pins as P
 import oracle_pins_fused as PF
+import oracle_pins_acc16 as PA
 
 # (name, text in oracle_gba.c, replacement) -- each a plausible slip.
 MUTANTS = [
@@ -62,7 +63,21 @@ MUTANTS += [
      "left_elem(J->layout_a, X, ldx, i, K - 1 - k, J->pro_relu)"),
 ]
 
-ALL_PINS = P.PINS + PF.PINS
+# Slips in the binary16 rounding and the fp16-accumulation reading.
+MUTANTS += [
+    ("round_truncates", "double r = rint(ldexp(ax, -q));", "double r = trunc(ldexp(ax, -q));"),
+    ("round_half_up", "double r = rint(ldexp(ax, -q));", "double r = floor(ldexp(ax, -q) + 0.5);"),
+    ("round_no_subnormal_floor", "    if (q < -24)\n        q = -24;\n", "    if (q < -30)\n        q = -30;\n"),
+    ("round_quantum_off_by_one", "int q = e - 11;", "int q = e - 10;"),
+    ("round_overflow_threshold", "if (ax >= 65520.0)", "if (ax > 65520.0)"),
+    ("acc16_group_16", "if (k % 32 == 31 || k == K - 1)", "if (k % 16 == 15 || k == K - 1)"),
+    ("acc16_group_misaligned", "if (k % 32 == 31 || k == K - 1)", "if (k % 32 == 0 || k == K - 1)"),
+    ("acc16_no_tail_rounding", "if (k % 32 == 31 || k == K - 1)", "if (k % 32 == 31)"),
+    ("acc16_round_only_at_end", "if (k % 32 == 31 || k == K - 1)", "if (k == K - 1)"),
+    ("acc16_second_not_subtracted", "J->second > 0 ? 1.0 : -1.0);", "1.0);"),
+]
+
+ALL_PINS = P.PINS + PF.PINS + PA.PINS
 
 
 def _build_mutant(tmp_path, name, old, new):
