@@ -596,29 +596,36 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
 
     // Epilogue on registers: +/- bias, activation, fp16, two 16-byte stores
     // per lane per 32x32 block (each guarded so an output shared with a
-    // neighbouring tile is stored by its owner only).
+    // neighbouring tile is stored by its owner only).  Row blocks outermost:
+    // a wave's consecutive stores complete each row of its warp tile (up to
+    // 128 bytes), so no cache line is written back to memory half-filled
+    // while the whole grid stores at once.
+    float b[TN][16];
 #pragma unroll
     for (int t = 0; t < TN; ++t) {
         const int j = nc + wn * WTN + 32 * t + 16 * hi;
-        float b[16];
         if (p.bias_kind == BIAS_ROW) {
             const h8 b0 = *reinterpret_cast<const h8 *>(p.bias + j);
             const h8 b1 = *reinterpret_cast<const h8 *>(p.bias + j + 8);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                b[e] = p.bias_sign * (float)b0[e];
-                b[8 + e] = p.bias_sign * (float)b1[e];
+                b[t][e] = p.bias_sign * (float)b0[e];
+                b[t][8 + e] = p.bias_sign * (float)b1[e];
             }
         } else {
 #pragma unroll
-            for (int e = 0; e < 16; ++e) b[e] = 0.f;
+            for (int e = 0; e < 16; ++e) b[t][e] = 0.f;
         }
+    }
 #pragma unroll
-        for (int s = 0; s < TM; ++s) {
+    for (int s = 0; s < TM; ++s) {
+#pragma unroll
+        for (int t = 0; t < TN; ++t) {
+            const int j = nc + wn * WTN + 32 * t + 16 * hi;
             const int i = mc + wm * WTM + 32 * s + l32;
             float x[16];
 #pragma unroll
-            for (int e = 0; e < 16; ++e) x[e] = acc[t][s][e] + b[e];
+            for (int e = 0; e < 16; ++e) x[e] = acc[t][s][e] + b[t][e];
             if (p.bias_kind == BIAS_FULL) {
                 const _Float16 *bp = p.bias + (int64_t)i * p.ldbias + j;
                 const h8 b0 = *reinterpret_cast<const h8 *>(bp);

@@ -63,12 +63,20 @@ class Problem:
                        act=ACT[act], rows=rows, acc16=acc16)
 
     def gpu(self, layout, prologue=False, second="add", bias_op="add", act="relu", accum="f32",
-            tile=None, pad=0, offset=False):
+            tile=None, pad=0, offset=False, ld=None, out=None):
         la, lb = D.LAYOUT_NAMES[layout]
 
         def dev(x, lay):
             if x is None:
                 return None
+            if ld is not None:
+                # every operand with leading dimension ld, built on the device
+                # (NaN padding, as in datagen.store)
+                rows, cols = x.shape
+                outer, inner = (rows, cols) if lay == D.ROW else (cols, rows)
+                t = torch.full((outer, ld), float("nan"), dtype=torch.float16, device="cuda")
+                t[:, :inner].copy_(torch.from_numpy(D.store(x, lay)).cuda())
+                return t[:, :cols] if lay == D.ROW else t[:, :rows].t()
             if not offset:
                 return U.device_operand(x, lay, pad)
             # storage shifted by one element: 2-byte aligned only (general path)
@@ -86,7 +94,7 @@ class Problem:
                      else dev(self.bias, D.ROW))
         o = gba.fused_gemm(dev(self.A, la), dev(self.B, lb), P=dev(self.P, la), Q=dev(self.Q, lb),
                            second=second, prologue="relu" if prologue else None, bias=dbias,
-                           bias_op=bias_op, act=act, accum=accum, tile=tile)
+                           bias_op=bias_op, act=act, accum=accum, tile=tile, out=out)
         torch.cuda.synchronize()
         return o.cpu().numpy()
 
@@ -257,6 +265,31 @@ def test_unaligned_operands_general_path(layout):
     kw = dict(prologue=True, second="sub", bias_op="add", act="tanh")
     U.assert_close(pr.gpu(layout, **kw, offset=True, pad=3), pr.oracle(**kw),
                    what=f"unaligned {layout}")
+
+
+# The fast path addresses each operand tile with 32-bit offsets and so takes
+# leading dimensions below 2^21 elements; larger ones go to the general path.
+# Both sides of that limit, every operand (and the full bias) at that leading
+# dimension, the output at a leading dimension above it.
+FAST_MAX_LD = 1 << 21
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("ld", [FAST_MAX_LD - 8, FAST_MAX_LD])
+def test_large_leading_dimensions(layout, ld):
+    pr = Problem(830, 300, 264, 264, K2=136, full_bias=True)
+    kw = dict(prologue=True, second="sub", bias_op="sub", act="relu")
+    ref = pr.oracle(**kw)
+    big = torch.full((pr.M, FAST_MAX_LD + 8), float("nan"), dtype=torch.float16, device="cuda")
+    out = big[:, :pr.N]
+    for tile in (None, 1, 11):
+        announce("large_ld", layout, ld, tile)
+        U.assert_close(pr.gpu(layout, **kw, tile=tile, ld=ld, out=out), ref,
+                       what=f"ld={ld} {layout} tile {tile}")
+        # the output's padding stays untouched
+        assert torch.isnan(big[:, pr.N:pr.N + 64]).all().item()
+    del big, out
+    torch.cuda.empty_cache()
 
 
 def test_gemm_bias_act_is_the_single_product_case():
