@@ -150,10 +150,42 @@ typedef struct gba_fused_desc {
     void *C;                      /* output, row-major: C[i*ldc + j], ldc >= N */
     int64_t ldc;
     int tile_id;                  /* < 0: library's choice; else as gemm_bias_act_tile */
+    int split_k;                  /* 0: library's choice, 1: never, s >= 2: s-way (see below) */
+    void *workspace;              /* device memory for a split reduction, or NULL */
+    size_t workspace_bytes;
 } gba_fused_desc;
 
-/* Set *desc to the defaults listed above (tile_id = -1).  NULL is ignored. */
+/* Set *desc to the defaults listed above (tile_id = -1, split_k = 0, no
+ * workspace, everything else zero / NONE / ADD / F32).  NULL is ignored. */
 void gba_fused_desc_init(gba_fused_desc *desc);
+
+/*
+ * gba_fused_workspace_size -- bytes of workspace the request would use to
+ * split its reduction across workgroups (0: it would not split).
+ *
+ * Splitting is an implementation choice of the fast path for fp32
+ * accumulation (the paper partitions the reduction only inside a thread
+ * block; this is the same partition across blocks): when an output has too
+ * few tiles to occupy the GPU, or a long reduction, each output tile's
+ * reduction steps (A.B's, then P.Q's) are divided among up to split_k
+ * workgroups.  Each writes its fp32 partial tile to the workspace; the last
+ * of a tile's splits to finish adds the partials in split order (the result
+ * does not depend on which finishes last) and runs the epilogue.  Only the
+ * summation order changes, not the tolerance; GBA_ACC_F16 never splits.
+ *
+ * Workspace contract (gba_fused_gemm): at least this many bytes, 256-byte
+ * aligned, on the device the call runs on.  It starts with one 32-bit
+ * counter per output tile that must be zero when the call is enqueued and
+ * is zero again when the call completes, so a workspace zero-filled once
+ * serves any number of calls in stream order; calls that may run at the
+ * same time need separate workspaces.  With a NULL or smaller workspace the
+ * call runs unsplit.  split_k >= 2 asks for that many splits (fewer when
+ * the reduction has fewer 64-deep steps); 0 lets the library decide.
+ *
+ * Errors: as gba_fused_gemm's validation; GBA_EINVAL also for bytes ==
+ * NULL or split_k < 0.
+ */
+gba_status gba_fused_workspace_size(const gba_fused_desc *desc, size_t *bytes);
 
 /*
  * gba_fused_gemm -- the four computation idioms of the paper's scope
@@ -187,10 +219,13 @@ void gba_fused_desc_init(gba_fused_desc *desc);
  *
  * Degenerate sizes: M == 0 or N == 0 -> GBA_OK, nothing launched; K == 0
  * or K2 == 0 make that product's empty sum zero.
+ * Reduction split across workgroups: see gba_fused_workspace_size.
+ *
  * Errors: GBA_EINVAL for desc == NULL, a bad enum, a tile_id at or beyond
  * gba_num_tiles(), negative sizes or leading dimensions, a leading
- * dimension below its extent, or a NULL pointer that the request reads
- * (A/B when K > 0, P/Q when K2 > 0, bias when bias_kind != NONE, C);
+ * dimension below its extent, a NULL pointer that the request reads
+ * (A/B when K > 0, P/Q when K2 > 0, bias when bias_kind != NONE, C),
+ * split_k < 0, or a workspace not 256-byte aligned;
  * GBA_EUNSUPPORTED for M, N, K or K2 above 2^31-1 or pointers not 2-byte
  * aligned; GBA_EHIP if the launch fails.  Nothing is launched on error.
  */

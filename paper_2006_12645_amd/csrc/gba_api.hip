@@ -29,6 +29,8 @@ gba_status validate(const gba_fused_desc &d)
     if (d.bias_kind < GBA_BIAS_NONE || d.bias_kind > GBA_BIAS_FULL) return GBA_EINVAL;
     if (d.bias_op != GBA_OP_ADD && d.bias_op != GBA_OP_SUB) return GBA_EINVAL;
     if (d.tile_id >= NUM_TILES) return GBA_EINVAL;
+    if (d.split_k < 0) return GBA_EINVAL;
+    if (d.workspace != nullptr && !aligned(d.workspace, 256)) return GBA_EINVAL;
     const bool two = has_second(d);
     if (d.M < 0 || d.N < 0 || d.K < 0 || d.lda < 0 || d.ldb < 0 || d.ldc < 0) return GBA_EINVAL;
     if (two && (d.K2 < 0 || d.ldp < 0 || d.ldq < 0)) return GBA_EINVAL;
@@ -132,21 +134,90 @@ const LayoutTable &table_for(int la, int lb, bool pro, bool dual)
     return lb == GBA_ROW_MAJOR ? variant_table<COL, ROW>(pro, dual) : variant_table<COL, COL>(pro, dual);
 }
 
+// Most workgroups one output tile's reduction is split across.
+constexpr int64_t MAX_SPLITS = 64;
+
+// The library splits a reduction by itself (split_k == 0) only where that
+// was measured to win: reductions of 16384 or more over so few outputs that
+// the 64x64 tile makes at most 32 workgroups.  There the 64x64 tile with
+// about 128 workgroups in all beats every unsplit tile 1.6-2.7x
+// (64x512x32768: 30 us against 50; 128x128x65536: 35 against 94).  On
+// shorter reductions the partial-tile traffic and the device-scope release
+// of every split cost more than the extra workgroups gain.
+constexpr int AUTO_SPLIT_TILE = 6;
+
+int64_t auto_splits(int64_t M, int64_t N, int64_t ktot)
+{
+    const TileCfg &c = TILES[AUTO_SPLIT_TILE];
+    if (ktot < 16384 || !tile_fits(AUTO_SPLIT_TILE, M, N)) return 1;
+    const int64_t tiles = ceil_div(M, c.bm) * ceil_div(N, c.bn);
+    return tiles <= 32 ? ceil_div(128, tiles) : 1;
+}
+
+// How a valid request runs: the tile (or the general path), the output tile
+// grid, and the split of each tile's reduction across workgroups with the
+// workspace it needs.
+struct Plan {
+    int tile;          // -1: general path
+    TileCfg cfg;
+    int64_t tiles_m, tiles_n;
+    int64_t splits, split_steps;
+    size_t ws_bytes;   // 0 when unsplit
+};
+
+size_t counter_bytes(int64_t tiles) { return (size_t)ceil_div(tiles * 4, 256) * 256; }
+
+Plan make_plan(const gba_fused_desc &d, bool may_split)
+{
+    const bool two = has_second(d);
+    const int64_t ktot = d.K + (two ? d.K2 : 0);
+    Plan pl;
+    // A requested tile that is larger than the problem is replaced by the
+    // library's choice; problems smaller than every tile take the general path.
+    const bool tile_ok = d.tile_id >= 0 && tile_fits(d.tile_id, d.M, d.N) &&
+                         !(d.accum == GBA_ACC_F16 && TILES[d.tile_id].sk > 1);
+    const bool fp32 = d.accum == GBA_ACC_F32;
+    int64_t auto_s = 1;
+    if (may_split && d.split_k == 0 && !tile_ok && fp32) auto_s = auto_splits(d.M, d.N, ktot);
+    pl.tile = tile_ok ? d.tile_id : (auto_s > 1 ? AUTO_SPLIT_TILE : select_tile(d.M, d.N, ktot, d.accum));
+    if (pl.tile >= 0 && !fast_path_ok(d)) pl.tile = -1;
+    pl.cfg = pl.tile >= 0 ? TILES[pl.tile] : GENERIC_TILE;
+    pl.tiles_m = ceil_div(d.M, pl.cfg.bm);
+    pl.tiles_n = ceil_div(d.N, pl.cfg.bn);
+    pl.splits = 1;
+    pl.split_steps = 0;
+    pl.ws_bytes = 0;
+    if (may_split && pl.tile >= 0 && tile_splits(pl.cfg) && fp32 && d.split_k != 1) {
+        const int64_t tiles = pl.tiles_m * pl.tiles_n;
+        const int64_t nk = ceil_div(d.K, 64) + (two ? ceil_div(d.K2, 64) : 0);
+        int64_t want = d.split_k >= 2 ? d.split_k : auto_s;
+        want = want < nk ? want : nk;
+        want = want < MAX_SPLITS ? want : MAX_SPLITS;
+        if (want >= 2) {
+            // equal step ranges, none of them empty
+            const int64_t steps = ceil_div(nk, want);
+            const int64_t splits = ceil_div(nk, steps);
+            if (splits >= 2 && tiles * splits <= INT_MAX) {
+                pl.splits = splits;
+                pl.split_steps = steps;
+                pl.ws_bytes = counter_bytes(tiles) + (size_t)(splits * tiles) * pl.cfg.bm * pl.cfg.bn * sizeof(float);
+            }
+        }
+    }
+    return pl;
+}
+
 gba_status run_fused(const gba_fused_desc &d, hipStream_t stream)
 {
     gba_status st = validate(d);
     if (st != GBA_OK || d.M == 0 || d.N == 0) return st;
     const bool two = has_second(d);
-    const int64_t ktot = d.K + (two ? d.K2 : 0);
-
-    // A requested tile that is larger than the problem is replaced by the
-    // library's choice; problems smaller than every tile take the general path.
-    const bool tile_ok = d.tile_id >= 0 && tile_fits(d.tile_id, d.M, d.N) &&
-                         !(d.accum == GBA_ACC_F16 && TILES[d.tile_id].sk > 1);
-    int tile = tile_ok ? d.tile_id : select_tile(d.M, d.N, ktot, d.accum);
-    const bool fast = tile >= 0 && fast_path_ok(d);
-    if (!fast) tile = -1;
-    const TileCfg cfg = fast ? TILES[tile] : GENERIC_TILE;
+    // Without room for the split the plan is made again without one (the
+    // library's unsplit tile choice differs from its split one).
+    Plan pl = make_plan(d, true);
+    if (pl.splits > 1 && (d.workspace == nullptr || d.workspace_bytes < pl.ws_bytes)) pl = make_plan(d, false);
+    const int tile = pl.tile;
+    const bool fast = tile >= 0;
 
     GemmArgs a;
     a.A = static_cast<const _Float16 *>(d.A);
@@ -169,13 +240,19 @@ gba_status run_fused(const gba_fused_desc &d, hipStream_t stream)
     a.bias_kind = d.bias_kind;
     a.bias_sign = d.bias_op == GBA_OP_SUB ? -1.f : 1.f;
     a.sub = d.second == GBA_SECOND_SUB;
-    a.tiles_m = (int)ceil_div(d.M, cfg.bm);
-    a.tiles_n = (int)ceil_div(d.N, cfg.bn);
-    if ((int64_t)a.tiles_m * a.tiles_n > INT_MAX) return GBA_EUNSUPPORTED;
+    if (pl.tiles_m * pl.tiles_n > INT_MAX) return GBA_EUNSUPPORTED;
+    a.tiles_m = (int)pl.tiles_m;
+    a.tiles_n = (int)pl.tiles_n;
+    a.splits = (int)pl.splits;
+    a.split_steps = (int)pl.split_steps;
+    a.counters = pl.splits > 1 ? static_cast<unsigned *>(d.workspace) : nullptr;
+    a.ws = pl.splits > 1 ? reinterpret_cast<float *>(static_cast<char *>(d.workspace) +
+                                                      counter_bytes(pl.tiles_m * pl.tiles_n))
+                         : nullptr;
 
     const LayoutTable &tab = table_for(d.layoutA, d.layoutB, d.prologue == GBA_PRO_RELU, two);
     const int acc16 = d.accum == GBA_ACC_F16;
-    LaunchFn fn = fast ? tab.fast[tile][acc16] : tab.generic[acc16];
+    LaunchFn fn = !fast ? tab.generic[acc16] : (pl.splits > 1 ? tab.split[tile] : tab.fast[tile][acc16]);
     return fn(a, stream) == hipSuccess ? GBA_OK : GBA_EHIP;
 }
 
@@ -316,6 +393,16 @@ extern "C" void gba_fused_desc_init(gba_fused_desc *desc)
     desc->act = GBA_ACT_NONE;
     desc->accum = GBA_ACC_F32;
     desc->tile_id = -1;
+}
+
+extern "C" gba_status gba_fused_workspace_size(const gba_fused_desc *desc, size_t *bytes)
+{
+    if (desc == nullptr || bytes == nullptr) return GBA_EINVAL;
+    *bytes = 0;
+    const gba_status st = validate(*desc);
+    if (st != GBA_OK || desc->M == 0 || desc->N == 0) return st;
+    *bytes = make_plan(*desc, true).ws_bytes;
+    return GBA_OK;
 }
 
 extern "C" gba_status gba_fused_gemm(const gba_fused_desc *desc, gba_stream_t stream)

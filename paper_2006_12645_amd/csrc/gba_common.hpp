@@ -35,6 +35,15 @@ struct GemmArgs {
     float bias_sign;       // +1: add the bias, -1: subtract it
     int sub;               // nonzero: C = A.B - P.Q instead of A.B + P.Q
     int tiles_m, tiles_n;
+    // Reduction split across workgroups (splits > 1): workgroup b computes
+    // split b % splits of output tile b / splits, i.e. reduction steps
+    // [split * split_steps, (split + 1) * split_steps) of the steps of A.B
+    // followed by those of P.Q; its fp32 partial tile goes to ws and the
+    // last split of a tile to arrive (counted in counters, which start and
+    // end at zero) sums them in split order and runs the epilogue.
+    int splits, split_steps;
+    float *ws;
+    unsigned *counters;
 };
 
 __device__ __forceinline__ h8 zero_h8()

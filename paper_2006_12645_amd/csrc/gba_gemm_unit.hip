@@ -19,12 +19,15 @@ constexpr bool UNIT_PRO = GBA_PRO != 0, UNIT_DUAL = GBA_DUAL != 0;
 #define GBA_FAST_ENTRY(id, BM, BN, WM, WN, SK, NSTG)                                              \
     {&launch_fast<BM, BN, WM, WN, SK, NSTG, UNIT_LA, UNIT_LB, false, UNIT_PRO, UNIT_DUAL>,         \
      fast_acc16<BM, BN, WM, WN, SK, NSTG, UNIT_LA, UNIT_LB, UNIT_PRO, UNIT_DUAL>()},
+#define GBA_SPLIT_ENTRY(id, BM, BN, WM, WN, SK, NSTG) \
+    fast_split<BM, BN, WM, WN, SK, NSTG, UNIT_LA, UNIT_LB, UNIT_PRO, UNIT_DUAL>(),
 
 template <>
 const LayoutTable &layout_table<UNIT_LA, UNIT_LB, UNIT_PRO, UNIT_DUAL>()
 {
     static const LayoutTable t = {
         {GBA_TILE_LIST(GBA_FAST_ENTRY)},
+        {GBA_TILE_LIST(GBA_SPLIT_ENTRY)},
         {&launch_generic<UNIT_LA, UNIT_LB, false, UNIT_PRO, UNIT_DUAL>,
          &launch_generic<UNIT_LA, UNIT_LB, true, UNIT_PRO, UNIT_DUAL>},
     };
@@ -32,5 +35,6 @@ const LayoutTable &layout_table<UNIT_LA, UNIT_LB, UNIT_PRO, UNIT_DUAL>()
 }
 
 #undef GBA_FAST_ENTRY
+#undef GBA_SPLIT_ENTRY
 
 }  // namespace gba

@@ -314,8 +314,12 @@ struct DmaCopy {
 // the same registers after A.B (Matmuls with Pointwise Epilogue
 // subsection): the reduction runs over A.B's K steps and then over P.Q's K2
 // steps, and only the sum (or difference) leaves the kernel.
+// SPLIT: each output tile's reduction is split across p.splits workgroups
+// (the grid holds p.splits workgroups per tile); every split writes its
+// fp32 partial tile to p.ws and the last one of a tile to arrive sums them
+// in split order and runs the epilogue.
 template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool DMA,
-          bool PRO, bool DUAL>
+          bool PRO, bool DUAL, bool SPLIT>
 __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs p)
 {
     constexpr int NTG = 64 * WM * WN;         // threads per k-group
@@ -347,8 +351,17 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
     const int wm = (wave % (WM * WN)) % WM, wn = (wave % (WM * WN)) / WM;
     const int l32 = lane & 31, hi = lane >> 5;
 
+    static_assert(!SPLIT || (SK == 1 && !ACC16), "a split reduction needs one k-group and fp32 sums");
+    // This workgroup's output tile and, under a split reduction, its split
+    // (readfirstlane: both are uniform, and in scalar registers every
+    // address derived from them stays scalar).
+    int tile_id = blockIdx.x, kspl = 0;
+    if constexpr (SPLIT) {
+        tile_id = __builtin_amdgcn_readfirstlane((int)blockIdx.x / p.splits);
+        kspl = __builtin_amdgcn_readfirstlane((int)blockIdx.x - tile_id * p.splits);
+    }
     int tm, tn;
-    tile_coords(blockIdx.x, gridDim.x, p.tiles_m, tm, tn);
+    tile_coords(tile_id, SPLIT ? p.tiles_m * p.tiles_n : (int)gridDim.x, p.tiles_m, tm, tn);
     // Output tile origin, and the origin of the tile actually computed: an
     // edge tile is shifted back so that it lies inside the matrix (M >= BM
     // and N >= BN on this path); the rows/columns it shares with its
@@ -465,7 +478,18 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
             if constexpr (LB == COL) return make_rsrc(Y + (int64_t)nc * ldy + k0, MAX_RECORDS);
             else return make_rsrc(Y + (int64_t)k0 * ldy + nc, MAX_RECORDS);
         };
-        const int nk = (Kseg + SK * BK - 1) / (SK * BK);
+        // Steps [s_lo, s_hi) of this product are this workgroup's: all of
+        // them, or under a split its part of the split's range of the
+        // concatenated steps of both products.
+        const int nk_seg = (Kseg + SK * BK - 1) / (SK * BK);
+        int s_lo = 0, s_hi = nk_seg;
+        if constexpr (SPLIT) {
+            const int off = seg == 0 ? 0 : (p.K + SK * BK - 1) / (SK * BK);
+            const int lo = kspl * p.split_steps - off, hi = lo + p.split_steps;
+            s_lo = __builtin_amdgcn_readfirstlane(lo < 0 ? 0 : (lo > nk_seg ? nk_seg : lo));
+            s_hi = __builtin_amdgcn_readfirstlane(hi < 0 ? 0 : (hi > nk_seg ? nk_seg : hi));
+        }
+        const int nk = s_hi - s_lo;
 
         // Copies of step s (this k-group's slab): direct-to-LDS operands into
         // `stage`, the others into their staging registers.  Steps past the
@@ -473,7 +497,11 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
         // every step of the loop below has the same shape.  A slab starting at
         // or beyond K reads as zeros.
         auto copy_step = [&](int s, char *stage) {
-            const int k0 = ((s < nk ? s : nk - 1) * SK + grp) * BK;
+            int k0 = (((s < nk ? s : nk - 1) + s_lo) * SK + grp) * BK;
+            // wave-uniform; without readfirstlane the compiler takes the
+            // k-group index (from the thread index) or the split range for
+            // divergent and loops over the lanes of every copy
+            if constexpr (SK > 1 || SPLIT) k0 = __builtin_amdgcn_readfirstlane(k0);
             const int kleft = Kseg - k0;
             const auto ra = rsrc_a(k0);
             const auto rb = rsrc_b(k0);
@@ -540,6 +568,66 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
         // when it is reused below or released.
         __builtin_amdgcn_s_waitcnt(0);
         if (seg == 1 && p.sub) negate_acc();
+    }
+
+    if constexpr (SPLIT) {
+        {
+            // Partial tile of this split to the workspace, each thread's
+            // accumulators of a 32x32 block as 16 consecutive floats (a wave
+            // writes 4 KB contiguously per block).
+            float *const part = p.ws + (size_t)tile_id * p.splits * (BM * BN);
+#pragma unroll
+            for (int t = 0; t < TN; ++t)
+#pragma unroll
+                for (int s = 0; s < TM; ++s) {
+                    f4 *dst = reinterpret_cast<f4 *>(part + (size_t)kspl * (BM * BN) + ((t * TM + s) * NT + tid) * 16);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        dst[q] = f4{acc[t][s][4 * q], acc[t][s][4 * q + 1], acc[t][s][4 * q + 2], acc[t][s][4 * q + 3]};
+                }
+            // Count this split in, releasing the workgroup's partial (all of
+            // its stores are done at the barrier) at device scope; the last
+            // split to arrive acquires every other split's partial and goes
+            // on, the others are done.  One release per workgroup and one
+            // acquire per output tile: an acquire invalidates the cached
+            // operands of every workgroup sharing the cache.
+            __syncthreads();
+            __shared__ int last_split;
+            if (tid == 0) {
+                const unsigned before = __hip_atomic_fetch_add(p.counters + tile_id, 1u, __ATOMIC_RELEASE,
+                                                               __HIP_MEMORY_SCOPE_AGENT);
+                last_split = before == (unsigned)(p.splits - 1);
+                if (last_split) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            }
+            __syncthreads();
+            if (!__builtin_amdgcn_readfirstlane(last_split)) return;
+            // Sum of the partials in split order (independent of arrival
+            // order, so the result is deterministic); the counter is reset
+            // for the next call.
+#pragma unroll
+            for (int t = 0; t < TN; ++t)
+#pragma unroll
+                for (int s = 0; s < TM; ++s)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) acc[t][s][e] = 0.f;
+            for (int j = 0; j < p.splits; ++j) {
+#pragma unroll
+                for (int t = 0; t < TN; ++t)
+#pragma unroll
+                    for (int s = 0; s < TM; ++s) {
+                        const f4 *src =
+                            reinterpret_cast<const f4 *>(part + (size_t)j * (BM * BN) + ((t * TM + s) * NT + tid) * 16);
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const f4 v = src[q];
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) acc[t][s][4 * q + e] += v[e];
+                        }
+                    }
+            }
+            if (tid == 0)
+                __hip_atomic_store(p.counters + tile_id, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
     }
 
     if constexpr (SK > 1) {

@@ -54,19 +54,28 @@ constexpr TileCfg GENERIC_TILE = {64, 64, 2, 2, 1, 2};
 
 typedef hipError_t (*LaunchFn)(const GemmArgs &, hipStream_t);
 
+// Tiles whose reduction can also be split across workgroups (fp32
+// accumulation): one k-group and at most 128x128 outputs.  Larger tiles
+// already fill the GPU with few output tiles.
+constexpr bool tile_splits(const TileCfg &c) { return c.sk == 1 && c.bm * c.bn <= 128 * 128; }
+
 // Per operand-layout pair and kernel variant: fast[tile][acc16] for the
-// aligned fast path (null for fp16 accumulation with split-K),
-// generic[acc16] otherwise.
+// aligned fast path (null for fp16 accumulation with split-K), split[tile]
+// for its reduction split across workgroups (null where tile_splits is
+// false), generic[acc16] otherwise.
 struct LayoutTable {
     LaunchFn fast[NUM_TILES][2];
+    LaunchFn split[NUM_TILES];
     LaunchFn generic[2];
 };
 
-template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool PRO, bool DUAL>
+template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool PRO, bool DUAL,
+          bool SPLIT = false>
 hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
 {
-    dim3 grid((unsigned)(a.tiles_m * a.tiles_n)), block(64 * WM * WN * SK);
-    hipLaunchKernelGGL((gemm_bias_act_fast<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, true, PRO, DUAL>), grid,
+    // one workgroup per output tile, times the splits of its reduction
+    dim3 grid((unsigned)(a.tiles_m * a.tiles_n * (SPLIT ? a.splits : 1))), block(64 * WM * WN * SK);
+    hipLaunchKernelGGL((gemm_bias_act_fast<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, true, PRO, DUAL, SPLIT>), grid,
                        block, 0, s, a);
     return hipGetLastError();
 }
@@ -76,6 +85,15 @@ template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool
 constexpr LaunchFn fast_acc16()
 {
     if constexpr (SK == 1) return &launch_fast<BM, BN, WM, WN, SK, NSTG, LA, LB, true, PRO, DUAL>;
+    else return nullptr;
+}
+
+// Launch-table entry for a reduction split across workgroups.
+template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool PRO, bool DUAL>
+constexpr LaunchFn fast_split()
+{
+    if constexpr (tile_splits(TileCfg{BM, BN, WM, WN, SK, NSTG}))
+        return &launch_fast<BM, BN, WM, WN, SK, NSTG, LA, LB, false, PRO, DUAL, true>;
     else return nullptr;
 }
 

@@ -36,7 +36,8 @@ class FusedDesc(ctypes.Structure):
                 ("prologue", _int), ("second", _int), ("K2", _i64),
                 ("P", _vp), ("ldp", _i64), ("Q", _vp), ("ldq", _i64),
                 ("bias_kind", _int), ("bias_op", _int), ("bias", _vp), ("ldbias", _i64),
-                ("act", _int), ("accum", _int), ("C", _vp), ("ldc", _i64), ("tile_id", _int)]
+                ("act", _int), ("accum", _int), ("C", _vp), ("ldc", _i64), ("tile_id", _int),
+                ("split_k", _int), ("workspace", _vp), ("workspace_bytes", ctypes.c_size_t)]
 
 
 # Every function include/gba.h declares, with its ctypes signature.
@@ -52,6 +53,7 @@ SIGNATURES = {
     "gba_add_f16": (_int, [_i64, _i64, _vp, _i64, _vp, _i64, _vp]),
     "gba_fused_desc_init": (None, [ctypes.POINTER(FusedDesc)]),
     "gba_fused_gemm": (_int, [ctypes.POINTER(FusedDesc), _vp]),
+    "gba_fused_workspace_size": (_int, [ctypes.POINTER(FusedDesc), ctypes.POINTER(ctypes.c_size_t)]),
     "gba_status_string": (_cp, [_int]),
     "gba_version": (_cp, []),
 }
@@ -164,8 +166,36 @@ def fused_gemm_desc(desc, stream=None, device=None):
     _check(lib().gba_fused_gemm(ctypes.byref(desc), _stream_handle(stream, device)), "gba_fused_gemm")
 
 
+def workspace_size(desc):
+    """Bytes of workspace a filled FusedDesc would use to split its reduction."""
+    n = ctypes.c_size_t(0)
+    _check(lib().gba_fused_workspace_size(ctypes.byref(desc), ctypes.byref(n)), "gba_fused_workspace_size")
+    return n.value
+
+
+# Zero-filled workspaces, one per (device, stream): the library leaves the
+# counters at their start zero after every call, so a workspace stays ready
+# for the next call in that stream's order.
+_workspaces = {}
+
+
+def stream_workspace(nbytes, device, stream=None):
+    """A zero-filled uint8 CUDA tensor of at least nbytes for calls on `stream`."""
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    key = (torch.device(device).index, stream.cuda_stream)
+    ws = _workspaces.get(key)
+    if ws is None or ws.numel() < nbytes:
+        with torch.cuda.stream(stream):
+            ws = torch.zeros(max(nbytes, 1 << 20), dtype=torch.uint8, device=device)
+        _workspaces[key] = ws
+    return ws
+
+
 def fused_gemm(A, B, *, P=None, Q=None, second="add", prologue=None, bias=None, bias_op="add",
-               act="relu", accum="f32", out=None, tile=None, stream=None):
+               act="relu", accum="f32", out=None, tile=None, split=None, workspace="auto",
+               stream=None):
     """out = act((pro(A) @ B  +/-  pro(P) @ Q)  +/-  bias) in one kernel.
 
     A (M, K), B (K, N): fp16 CUDA tensors, row- or column-major.  P (M, K2)
@@ -173,7 +203,10 @@ def fused_gemm(A, B, *, P=None, Q=None, second="add", prologue=None, bias=None, 
     "add" or "sub".  prologue: None or "relu" (applied to A and P).  bias:
     None, an (N,) vector or a row-major (M, N) matrix; ``bias_op`` "add" or
     "sub".  act: "none", "relu", "sigmoid", "tanh".  out: (M, N) row-major
-    fp16, allocated when None.
+    fp16, allocated when None.  split: None (library's choice) or the number
+    of workgroups each output tile's reduction is split across (1: never).
+    workspace: "auto" (a cached zero-filled buffer for this stream), None
+    (no split), or a zero-filled uint8 CUDA tensor owned by the caller.
     """
     import torch
     M, K = A.shape
@@ -232,6 +265,14 @@ def fused_gemm(A, B, *, P=None, Q=None, second="add", prologue=None, bias=None, 
         raise ValueError("out must be an (M, N) matrix")
     d.C, d.ldc = out.data_ptr(), _row_major_ld(out, "out")
     d.tile_id = -1 if tile is None else int(tile)
+    d.split_k = 0 if split is None else int(split)
+    if workspace is not None:
+        need = workspace_size(d)
+        if need > 0:
+            ws = stream_workspace(need, A.device, stream) if isinstance(workspace, str) else workspace
+            if ws.dtype != torch.uint8 or not ws.is_cuda:
+                raise TypeError("workspace must be a uint8 CUDA tensor")
+            d.workspace, d.workspace_bytes = ws.data_ptr(), ws.numel()
     fused_gemm_desc(d, stream, A.device)
     return out
 

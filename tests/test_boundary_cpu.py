@@ -173,8 +173,9 @@ def test_fused_desc_matches_c_layout(tmp_path):
 def test_fused_desc_defaults():
     d = gba.new_desc()
     assert (d.layoutA, d.layoutB, d.prologue, d.second, d.bias_kind, d.bias_op, d.act,
-            d.accum, d.tile_id) == (0, 0, 0, 0, 0, 0, 0, 0, -1)
+            d.accum, d.tile_id, d.split_k) == (0, 0, 0, 0, 0, 0, 0, 0, -1, 0)
     assert d.A is None and d.C is None and d.M == 0 and d.K2 == 0
+    assert d.workspace is None and d.workspace_bytes == 0
     gba.lib().gba_fused_desc_init(None)  # ignored, no crash
 
 
@@ -222,6 +223,9 @@ def fused(**kw):
     (dict(second=0, P=None, Q=None, K2=-7, ldp=-1, M=0), gba.GBA_OK),
     (dict(bias_kind=gba.GBA_BIAS_ROW, ldbias=-3, N=0), gba.GBA_OK),
     (dict(M=0, A=None, B=None, P=None, Q=None, C=None, bias=None), gba.GBA_OK),
+    (dict(split_k=-1), gba.GBA_EINVAL),
+    (dict(workspace=FAKE + 16, workspace_bytes=1 << 20), gba.GBA_EINVAL),
+    (dict(split_k=-1, M=0), gba.GBA_EINVAL),
 ])
 def test_fused_validation(kw, status):
     assert fused(**kw) == status
@@ -229,6 +233,84 @@ def test_fused_validation(kw, status):
 
 def test_fused_validation_null_desc():
     assert gba.lib().gba_fused_gemm(None, None) == gba.GBA_EINVAL
+
+
+def ws_bytes(**kw):
+    """gba_fused_workspace_size of an aligned one-product RC request
+    (M = N = 512, K = 320: five 64-deep steps), modified by kw."""
+    d = gba.new_desc()
+    d.layoutA, d.layoutB, d.M, d.N, d.K = 0, 1, 512, 512, 320
+    d.A, d.lda, d.B, d.ldb, d.C, d.ldc = FAKE, 320, FAKE, 320, FAKE, 512
+    for k, v in kw.items():
+        setattr(d, k, v)
+    n = ctypes.c_size_t(12345)
+    st = gba.lib().gba_fused_workspace_size(ctypes.byref(d), ctypes.byref(n))
+    return st, n.value
+
+
+def expected_ws(tile, M, N, splits):
+    info = gba.tile_info(tile)
+    tiles = -(-M // info["bm"]) * -(-N // info["bn"])
+    return -(-tiles * 4 // 256) * 256 + splits * tiles * info["bm"] * info["bn"] * 4
+
+
+@pytest.mark.parametrize("tile,split_k,splits", [
+    (4, 2, 2),    # 5 steps: ranges of 3 and 2
+    (4, 3, 3),    # ranges of 2, 2, 1
+    (4, 4, 3),    # ranges of 2 cover the 5 steps in 3 splits
+    (4, 5, 5),
+    (4, 9, 5),    # no more splits than steps
+    (6, 2, 2),
+    (9, 5, 5),
+])
+def test_workspace_size_of_forced_splits(tile, split_k, splits):
+    assert ws_bytes(tile_id=tile, split_k=split_k) == (gba.GBA_OK, expected_ws(tile, 512, 512, splits))
+
+
+@pytest.mark.parametrize("kw", [
+    dict(tile_id=4, split_k=1),                  # never split
+    dict(tile_id=10, split_k=4),                 # a tile with k-groups inside the workgroup
+    dict(tile_id=1, split_k=4),                  # 256x256: no split variant
+    dict(tile_id=4, split_k=4, accum=gba.GBA_ACC_F16),
+    dict(tile_id=4, split_k=4, A=FAKE + 2),      # general path
+    dict(tile_id=4, split_k=4, K=0),             # no reduction steps
+    dict(tile_id=4, split_k=4, K=64),            # one step
+    dict(tile_id=4, split_k=4, M=0),             # empty output
+])
+def test_workspace_size_without_split(kw):
+    assert ws_bytes(**kw) == (gba.GBA_OK, 0)
+
+
+@pytest.mark.parametrize("M,N,K,splits", [
+    (64, 512, 32768, 16),      # 8 tiles of 64x64: 128 workgroups
+    (128, 128, 65536, 32),     # 4 tiles
+    (64, 2048, 16384, 4),      # 32 tiles
+    (64, 2048, 16320, 0),      # reduction below 16384: no split
+    (512, 512, 32768, 0),      # 64 tiles: enough workgroups unsplit
+    (32, 512, 32768, 0),       # smaller than the 64x64 tile
+])
+def test_workspace_size_of_the_library_split(M, N, K, splits):
+    st, n = ws_bytes(M=M, N=N, K=K, lda=K, ldb=K, ldc=N)
+    assert (st, n) == (gba.GBA_OK, expected_ws(6, M, N, splits) if splits else 0)
+    # never for fp16 accumulation or a requested tile
+    assert ws_bytes(M=M, N=N, K=K, lda=K, ldb=K, ldc=N, accum=gba.GBA_ACC_F16) == (gba.GBA_OK, 0)
+    assert ws_bytes(M=M, N=N, K=K, lda=K, ldb=K, ldc=N, tile_id=8) == (gba.GBA_OK, 0)
+
+
+def test_workspace_size_counts_both_products():
+    # 5 + 3 steps of A.B and P.Q split 4 ways: ranges of 2
+    st, n = ws_bytes(tile_id=4, split_k=4, second=gba.GBA_SECOND_SUB, K2=192, P=FAKE, ldp=192,
+                     Q=FAKE, ldq=192)
+    assert (st, n) == (gba.GBA_OK, expected_ws(4, 512, 512, 4))
+
+
+def test_workspace_size_errors():
+    assert ws_bytes(split_k=-2)[0] == gba.GBA_EINVAL
+    assert ws_bytes(act=9)[0] == gba.GBA_EINVAL
+    d = gba.new_desc()
+    assert gba.lib().gba_fused_workspace_size(ctypes.byref(d), None) == gba.GBA_EINVAL
+    n = ctypes.c_size_t(0)
+    assert gba.lib().gba_fused_workspace_size(None, ctypes.byref(n)) == gba.GBA_EINVAL
 
 
 def test_generalised_act_enum_accepted_by_gemm_bias_act():

@@ -63,7 +63,7 @@ class Problem:
                        act=ACT[act], rows=rows, acc16=acc16)
 
     def gpu(self, layout, prologue=False, second="add", bias_op="add", act="relu", accum="f32",
-            tile=None, pad=0, offset=False, ld=None, out=None):
+            tile=None, pad=0, offset=False, ld=None, out=None, **extra):
         la, lb = D.LAYOUT_NAMES[layout]
 
         def dev(x, lay):
@@ -94,7 +94,7 @@ class Problem:
                      else dev(self.bias, D.ROW))
         o = gba.fused_gemm(dev(self.A, la), dev(self.B, lb), P=dev(self.P, la), Q=dev(self.Q, lb),
                            second=second, prologue="relu" if prologue else None, bias=dbias,
-                           bias_op=bias_op, act=act, accum=accum, tile=tile, out=out)
+                           bias_op=bias_op, act=act, accum=accum, tile=tile, out=out, **extra)
         torch.cuda.synchronize()
         return o.cpu().numpy()
 
@@ -290,6 +290,95 @@ def test_large_leading_dimensions(layout, ld):
         assert torch.isnan(big[:, pr.N:pr.N + 64]).all().item()
     del big, out
     torch.cuda.empty_cache()
+
+
+# ----------------------------------------------------------------------------
+# Reduction split across workgroups (partials in a workspace, summed by the
+# last split of each tile)
+
+def split_workspace(nbytes=64 << 20):
+    return torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+
+
+def counters_zero(ws, tile, M, N):
+    """The per-tile counters at the start of the workspace are back at 0."""
+    info = gba.tile_info(tile)
+    tiles = -(-M // info["bm"]) * -(-N // info["bn"])
+    return not ws[:tiles * 4].any().item()
+
+
+@pytest.mark.parametrize("tile", [4, 5, 6, 7, 8, 9])
+@pytest.mark.parametrize("split", [2, 3, 7])
+def test_split_reduction_all_features(tile, split):
+    # 16 + 4 steps of A.B and P.Q, ragged output (shifted edge tiles)
+    announce("split", tile, split)
+    pr = Problem(840, 300, 264, 1000, K2=200, full_bias=True)
+    kw = dict(prologue=True, second="sub", bias_op="sub", act="tanh")
+    ws = split_workspace()
+    U.assert_close(pr.gpu("RC", **kw, tile=tile, split=split, workspace=ws), pr.oracle(**kw),
+                   what=f"tile {tile} split {split}")
+    assert counters_zero(ws, tile, 300, 264), "split counters not reset"
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_split_reduction_layouts(layout):
+    announce("split_layouts", layout)
+    pr = Problem(841, 256, 320, 704, K2=136)
+    kw = dict(prologue=False, second="add", act="relu")
+    U.assert_close(pr.gpu(layout, **kw, tile=6, split=4, workspace=split_workspace()), pr.oracle(**kw),
+                   what=f"split {layout}")
+
+
+@pytest.mark.parametrize("split", [2, 3, 5, 16])
+def test_split_integer_exact(split):
+    announce("split_int", split)
+    pr = Problem(842, 200, 136, 1024, K2=64, dist="int")
+    kw = dict(second="sub", act="none")
+    got = pr.gpu("RC", **kw, tile=6, split=split, workspace=split_workspace())
+    assert np.array_equal(got.astype(np.float64), pr.oracle(**kw))
+
+
+def test_split_deterministic_and_reusable():
+    announce("split_repeat")
+    pr = Problem(843, 512, 512, 2048)
+    ws = split_workspace()
+    first = pr.gpu("RC", tile=4, split=8, workspace=ws)
+    for _ in range(3):
+        assert np.array_equal(pr.gpu("RC", tile=4, split=8, workspace=ws), first)
+    assert counters_zero(ws, 4, 512, 512)
+    U.assert_close(first, pr.oracle(), what="split 8")
+
+
+def test_split_workspace_reused_with_new_data():
+    # a second problem through the same workspace reads its own partials,
+    # not the first one's
+    announce("split_reuse")
+    ws = split_workspace()
+    first, second = Problem(846, 256, 192, 1536), Problem(847, 256, 192, 1536)
+    first.gpu("RC", tile=6, split=6, workspace=ws)
+    U.assert_close(second.gpu("RC", tile=6, split=6, workspace=ws), second.oracle(), what="reuse")
+    assert counters_zero(ws, 6, 256, 192)
+
+
+def test_library_split_on_long_reduction():
+    # 64 x 512 outputs over K = 32768: the library splits each 64x64 tile's
+    # reduction 16 ways when given a workspace, and runs unsplit without one
+    announce("library_split")
+    pr = Problem(848, 64, 512, 32768)
+    ref = pr.oracle()
+    U.assert_close(pr.gpu("RC"), ref, what="auto split")
+    U.assert_close(pr.gpu("RC", workspace=None), ref, what="no workspace")
+
+
+def test_split_needs_a_workspace():
+    # without a workspace (or with split 1) the call runs unsplit: same
+    # bits as the unsplit kernel
+    announce("split_no_ws")
+    pr = Problem(844, 256, 256, 512)
+    plain = pr.gpu("RC", tile=6, split=1)
+    assert np.array_equal(pr.gpu("RC", tile=6, split=4, workspace=None), plain)
+    split = pr.gpu("RC", tile=6, split=4, workspace=split_workspace())
+    U.assert_close(split, pr.oracle(), what="split 4")
 
 
 def test_gemm_bias_act_is_the_single_product_case():
