@@ -64,16 +64,22 @@ bool tile_fits(int tile, int64_t M, int64_t N) { return M >= TILES[tile].bm && N
 // sweeps of every tile, RC layout, fp32 accumulation):
 //   * the 256x256 tile (8 waves) as soon as it yields 136 workgroups: one
 //     round over 53% or more of the 256 compute units beats two rounds of
-//     a smaller tile;
+//     a smaller tile; from 112 when 128x128 tiles (two per compute unit)
+//     would not fit in one round;
 //   * else 128x128 (two workgroups per compute unit) from 260 workgroups,
 //     then 128x64 / 64x128 (the long side along the longer output side)
 //     from 400;
-//   * a long reduction (fp32 accumulation only) whose 64x64 tiles fit in
-//     one round of 88 to 256 workgroups takes 64x64 with two k-groups of
-//     waves (intra-workgroup split-K); with fewer output tiles still, 64x64
-//     with two k-groups while that makes more than 64 workgroups, else
-//     32x32 with four k-groups and four LDS stages;
-//   * else 64x64 from 200 workgroups, then 32x64, then 32x32.
+//   * a reduction of 1024 or more (fp32 accumulation only) whose 64x64
+//     tiles fit in one round of 160 (from K = 2048: 88) to 256 workgroups
+//     takes 64x64 with two k-groups of waves (intra-workgroup split-K);
+//     from K = 2048, with fewer
+//     output tiles still, 64x64 with two k-groups while that makes more
+//     than 64 workgroups, else 32x32 with four k-groups and four LDS
+//     stages;
+//   * else 64x64 from 200 workgroups, then 32x64 -- replaced, for fp32
+//     accumulation and K >= 768, by 32x32 with four k-groups when that
+//     makes at most 128 workgroups, else by 32x64 with four k-groups when
+//     that makes at most 256 -- then 32x32.
 // The 256x128 and 128x256 tiles were never the fastest in those sweeps and
 // are only used when asked for.
 int select_tile(int64_t M, int64_t N, int64_t K, int accum)
@@ -82,20 +88,29 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum)
         return tile_fits(t, M, N) ? ceil_div(M, TILES[t].bm) * ceil_div(N, TILES[t].bn) : 0;
     };
     if (tiles(1) >= 136) return 1;
+    if (tiles(1) >= 112 && tiles(4) > 512) return 1;  // 128x128 would need a second round
     if (tiles(4) >= 260) return 4;
     const int t57 = N > M ? 7 : 5;
     if (tiles(t57) >= 400) return t57;
-    if (accum == GBA_ACC_F32 && K >= 2048) {
+    if (accum == GBA_ACC_F32 && K >= 1024) {
         const int64_t n11 = tiles(11), n8 = tiles(8);
-        if (n11 >= 88 && n11 <= 256) return 11;
-        if (n8 < 128 || (K >= 4096 && n8 <= 128)) {
+        if (n11 >= (K >= 2048 ? 88 : 160) && n11 <= 256) return 11;
+        if (K >= 2048 && (n8 < 128 || (K >= 4096 && n8 <= 128))) {
             if (n11 > 64) return 11;
             if (tile_fits(13, M, N)) return 13;
         }
     }
     if (tiles(6) >= 200) return 6;
-    for (int t : {8, 9})
-        if (tile_fits(t, M, N)) return t;
+    if (tile_fits(8, M, N)) {
+        // few 32x64 tiles over a reduction of 768 or more: the k-group
+        // tiles keep more waves busy per output tile
+        if (accum == GBA_ACC_F32 && K >= 768) {
+            if (tile_fits(13, M, N) && tiles(13) <= 128) return 13;
+            if (tiles(12) <= 256) return 12;
+        }
+        return 8;
+    }
+    if (tile_fits(9, M, N)) return 9;
     return -1;  // smaller than the smallest tile: general path
 }
 
