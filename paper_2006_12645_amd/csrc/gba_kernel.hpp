@@ -497,11 +497,11 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
         // every step of the loop below has the same shape.  A slab starting at
         // or beyond K reads as zeros.
         auto copy_step = [&](int s, char *stage) {
-            int k0 = (((s < nk ? s : nk - 1) + s_lo) * SK + grp) * BK;
-            // wave-uniform; without readfirstlane the compiler takes the
-            // k-group index (from the thread index) or the split range for
-            // divergent and loops over the lanes of every copy
-            if constexpr (SK > 1 || SPLIT) k0 = __builtin_amdgcn_readfirstlane(k0);
+            // wave-uniform; without readfirstlane the compiler may take it
+            // (through the k-group index, from the thread index, or the
+            // split range) for divergent and loop over the lanes of every
+            // copy
+            const int k0 = __builtin_amdgcn_readfirstlane((((s < nk ? s : nk - 1) + s_lo) * SK + grp) * BK);
             const int kleft = Kseg - k0;
             const auto ra = rsrc_a(k0);
             const auto rb = rsrc_b(k0);
