@@ -296,6 +296,98 @@ struct DmaCopy {
     __device__ __forceinline__ void write(char *) {}
 };
 
+// LDS layout of an operand tile that is contiguous along M (column-major A)
+// or N (row-major B): 64 reduction rows of R elements, row k at byte 2Rk of
+// the tile, its 32-element block b kept at block position b ^ bswT<R>(k % 4).
+// The transposing fragment reads (ds_read_b64_tr_b16) of a wave touch four
+// consecutive rows and 4 x 16 bytes of one 32-element block per row half;
+// the block swizzle spreads those over all banks.
+template <int R>
+__device__ __forceinline__ int bswT(int j)
+{
+    if constexpr (R >= 128) return j;
+    else if constexpr (R == 64) return (j >> 1) & 1;
+    else return 0;
+}
+
+// Direct global -> LDS copy of such a tile (the transposed counterpart of
+// DmaCopy): instruction g = NW * i + w fills the g-th KB of the tile, i.e.
+// rows RPI * g .. RPI * g + RPI - 1, lane l the 16-byte chunk at byte 16 l,
+// fetched from the global chunk that the block swizzle puts there.  Rows at
+// or beyond K are fetched with an out-of-range offset and become zeros.
+template <int R, int NT>
+struct DmaCopyT {
+    static constexpr int NW = NT / 64;
+    static constexpr int CPR = R / 8;             // 16-byte chunks per row
+    static constexpr int RPI = 1024 / (2 * R);    // rows per instruction
+    static constexpr int NI = 64 / (RPI * NW);    // instructions per wave per step
+    static constexpr int NLOAD = NI;
+    static constexpr int NWRITE = 0;
+    static_assert(R >= 32 && R <= 512 && (R & (R - 1)) == 0, "rows of 32 to 512 elements");
+    static_assert(64 % (RPI * NW) == 0, "rows must divide evenly among the waves");
+
+    int voff[NI];  // lane byte offset from the instruction's first row
+    int krow[NI];  // reduction row (inside the step) of the lane's chunk
+    int w;         // wave index (uniform)
+    int64_t ldb2;
+
+    __device__ __forceinline__ void init(int64_t ld, int tid)
+    {
+        ldb2 = ld * 2;
+        w = __builtin_amdgcn_readfirstlane(tid >> 6);
+        const int l = tid & 63, rl = l / CPR, p = l % CPR;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int r = (NW * i + w) * RPI + rl;
+            const int col = 32 * ((p >> 2) ^ bswT<R>(r & 3)) + 8 * (p & 3);
+            voff[i] = (int)(rl * ldb2) + 2 * col;
+            krow[i] = r;
+        }
+    }
+
+    __device__ __forceinline__ void dma(__amdgpu_buffer_rsrc_t rs, char *stage, int kleft)
+    {
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int g = NW * i + w;
+            buffer_load16_lds(rs, stage + g * 1024, krow[i] < kleft ? voff[i] : OOB_OFFSET,
+                              (int)(g * RPI * ldb2));
+        }
+    }
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t, int) {}
+    __device__ __forceinline__ void write(char *) {}
+};
+
+// Lane byte offset, inside such a tile, of the first transposing read of the
+// fragment of 32-element block blk for the 16-deep slice at row 0 (add 32 R
+// bytes per slice, 8 R for the second read of four more rows).  A
+// ds_read_b64_tr_b16 gives lane 4c + d of every 16-lane group element d of
+// the 4-element chunk addressed by lane 4j + c, for j = 0..3: so lane 4j + c
+// addresses row j (plus 8 for the upper half-wave, which takes k 8..15 of
+// the slice) at the 4-column group that its result lanes 4c..4c+3 need.
+// PERM: the MFMA column order jp32 of the B operand (groups of four columns
+// stay together under it), else the identity.
+template <int R, bool PERM>
+__device__ __forceinline__ int offT(int lane, int blk)
+{
+    const int i = lane & 15, q = (lane >> 4) & 1, hi = lane >> 5;
+    const int j = i >> 2, c = i & 3;
+    const int colb = PERM ? 16 * (c & 1) + 8 * q + 4 * (c >> 1) : 16 * q + 4 * c;
+    return (8 * hi + j) * (2 * R) + 64 * (blk ^ bswT<R>(j)) + 16 * (colb >> 3) + 8 * ((colb >> 2) & 1);
+}
+
+typedef short s4v __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s4v lds_s4v;
+
+// The 8 fp16 of one fragment (rows k .. k+3 at p, k+4 .. k+7 at p + 8R).
+template <int R>
+__device__ __forceinline__ h8 read_frag_tr(const char *p)
+{
+    const s4v lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4v *)p);
+    const s4v hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4v *)(p + 8 * R));
+    return __builtin_bit_cast(h8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
 // SK > 1: intra-workgroup split-K (Split-K subsection): the workgroup holds
 // SK groups of WM x WN waves; in every step group g multiplies its own
 // 64-deep slab of the reduction (SK slabs per step, each in its own LDS
@@ -330,8 +422,12 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
     constexpr int ROWB = BK * 2;              // bytes per LDS row
     constexpr int SUB = (BM + BN) * ROWB;     // bytes per k-group sub-stage
     constexpr int STAGE = SK * SUB;           // bytes per LDS stage
-    constexpr bool DMA_A = DMA && LA == ROW;  // A copied straight into LDS
-    constexpr bool DMA_B = DMA && LB == COL;
+    // Operands contiguous along the reduction use DmaCopy and ds_read_b128
+    // fragments, the others DmaCopyT and transposing reads (TA / TB); with
+    // DMA false the latter are register-staged and transposed before the
+    // LDS write instead.
+    constexpr bool TA = DMA && LA == COL, TB = DMA && LB == ROW;
+    constexpr bool DMA_A = DMA, DMA_B = DMA;  // copied straight into LDS
     constexpr bool DEEP = DMA_A && DMA_B;
     constexpr int NS = DEEP ? NSTG : 2;       // LDS stages
     static_assert((NS & (NS - 1)) == 0, "stage count must be a power of two");
@@ -371,8 +467,10 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
     const int nc = n0 + BN <= p.N ? n0 : p.N - BN;
 
     constexpr bool FRAG_RELU = PRO && DMA_A;  // ReLU on fragments (no register stage)
-    using CopyA = std::conditional_t<DMA_A, DmaCopy<BM, NTG>, RegCopy<BM, NTG, LA == ROW, PRO>>;
-    using CopyB = std::conditional_t<DMA_B, DmaCopy<BN, NTG>, RegCopy<BN, NTG, LB == COL, false>>;
+    using CopyA = std::conditional_t<
+        DMA_A, std::conditional_t<TA, DmaCopyT<BM, NTG>, DmaCopy<BM, NTG>>, RegCopy<BM, NTG, LA == ROW, PRO>>;
+    using CopyB = std::conditional_t<
+        DMA_B, std::conditional_t<TB, DmaCopyT<BN, NTG>, DmaCopy<BN, NTG>>, RegCopy<BN, NTG, LB == COL, false>>;
     CopyA ca;
     CopyB cb;
 
@@ -388,6 +486,17 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
             offp[ks] = rp * ROWB + (((2 * ks + hi) ^ swz32(jp32(l32))) * 16);
         }
     }
+    // Transposing reads: per 32-element block of the warp tile (the B tile
+    // starts BM * ROWB bytes into the stage, as in the other layout).
+    int offtq[TA ? TM : 1], offtp[TB ? TN : 1];
+    if constexpr (TA) {
+#pragma unroll
+        for (int s = 0; s < TM; ++s) offtq[s] = offT<BM, false>(lane, wm * TM + s);
+    }
+    if constexpr (TB) {
+#pragma unroll
+        for (int t = 0; t < TN; ++t) offtp[t] = BM * ROWB + offT<BN, true>(lane, wn * TN + t);
+    }
 
     f16v acc[TN][TM];
 #pragma unroll
@@ -401,9 +510,15 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
     h8 fq[2][TM], fp[2][TN];
     auto read_frags = [&](int buf, const char *stage, int ks) {
 #pragma unroll
-        for (int s = 0; s < TM; ++s) fq[buf][s] = *reinterpret_cast<const h8 *>(stage + offq[ks] + s * 32 * ROWB);
+        for (int s = 0; s < TM; ++s) {
+            if constexpr (TA) fq[buf][s] = read_frag_tr<BM>(stage + offtq[s] + ks * 32 * BM);
+            else fq[buf][s] = *reinterpret_cast<const h8 *>(stage + offq[ks] + s * 32 * ROWB);
+        }
 #pragma unroll
-        for (int t = 0; t < TN; ++t) fp[buf][t] = *reinterpret_cast<const h8 *>(stage + offp[ks] + t * 32 * ROWB);
+        for (int t = 0; t < TN; ++t) {
+            if constexpr (TB) fp[buf][t] = read_frag_tr<BN>(stage + offtp[t] + ks * 32 * BN);
+            else fp[buf][t] = *reinterpret_cast<const h8 *>(stage + offp[ks] + t * 32 * ROWB);
+        }
     };
     auto mfmas = [&](int buf) {
         if constexpr (FRAG_RELU) {
@@ -441,7 +556,7 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
     // with the fragment read (DS read), staging write (DS write) or global
     // load (VMEM read) that has to overlap it.
     constexpr int NM = TN * TM;           // MFMAs per 16-deep slice
-    constexpr int NR = TM + TN;           // fragment reads per slice
+    constexpr int NR = TM * (TA ? 2 : 1) + TN * (TB ? 2 : 1);  // fragment reads per slice
     constexpr int NW = CopyA::NWRITE + CopyB::NWRITE;
     constexpr int NL = CopyA::NLOAD + CopyB::NLOAD;
     // Global loads still allowed in flight at the barrier of step kt: the
