@@ -8,11 +8,12 @@
 //   * A workgroup owns a BM x BN block tile of C, its WM x WN waves a
 //     (BM/WM) x (BN/WN) warp tile each; the reduction runs in steps of
 //     BK = 64 (strip-mining of the sequential dimension).
-//   * Each step's A and B tiles go global -> registers -> LDS (the split copy
-//     of the Global to Shared Memory subsection) through 16-byte buffer
-//     loads; the next step's loads are in flight while the current step is
-//     multiplied (Prefetching and Hiding Latency subsection) and LDS is
-//     double-buffered, so one barrier per step suffices.
+//   * Each step's A and B tiles go from global memory straight into LDS
+//     (gfx950's buffer loads with an LDS destination: the split copy of the
+//     Global to Shared Memory subsection without the register stage), in
+//     16-byte chunks; the copies of the next steps are in flight while the
+//     current step is multiplied (Prefetching and Hiding Latency subsection)
+//     over two or four LDS stages, with one barrier per step.
 //   * The wave-level contraction is v_mfma_f32_32x32x16_f16: fp16 inputs,
 //     fp32 accumulation, a 32x32 output block per instruction -- the CDNA4
 //     counterpart of the paper's 32x32x8 macro-MMA.  A 16-deep slice of k is
@@ -31,17 +32,18 @@
 // columns are consecutive -- the wide-store reordering that the paper does
 // through shared memory, obtained here for free.
 //
-// LDS.  Both tiles are stored reduction-contiguous, one 128-byte row (64
-// fp16 = 8 chunks of 16 bytes) per output row / column; chunk c of row r is
-// kept at chunk position c ^ swz32(r) (Swizzled Shared Memory subsection).
-// swz32 depends on r mod 32 only, so fragment addresses differ between
-// blocks by constants, and it makes the fragment reads and the row-wise
-// staging writes free of bank conflicts.
-//
-// Layouts.  A reduction-contiguous operand (row-major A, column-major B) is
-// copied chunk by chunk.  For the other two cases a lane loads an 8 x 8
-// block of fp16 as 8 chunks along M (or N), transposes it in registers and
-// writes 8 reduction-contiguous chunks: the per-layout copy helpers.
+// LDS and layouts.  Each tile keeps the layout it has in global memory.  A
+// reduction-contiguous operand (row-major A, column-major B) is stored as
+// one 128-byte row (64 fp16 = 8 chunks of 16 bytes) per output row / column,
+// chunk c of row r at chunk position c ^ swz32(r) (Swizzled Shared Memory
+// subsection), and its MFMA fragments are 16-byte reads.  An operand
+// contiguous along M or N (column-major A, row-major B) is stored as 64
+// reduction rows, block-swizzled (bswT), and its fragments come from
+// gfx950's transposing LDS reads (ds_read_b64_tr_b16), which turn four
+// rows of four consecutive elements into four elements of one column per
+// lane -- the transposition the paper's Volta kernels leave to the layout of
+// shared memory.  Both swizzles keep the fragment reads free of bank
+// conflicts; the copies write whole KB blocks of LDS.
 //
 // Edges.  A tile that would cross the last row or column of C is shifted
 // back inside the matrix (this path needs M >= BM and N >= BN), so its loads
@@ -83,108 +85,6 @@ __device__ __forceinline__ int swz32(int r)
 // lane, which this maps to column 16*(lane/32) + r.
 __device__ __forceinline__ int jp32(int rho) { return 16 * ((rho >> 2) & 1) + 4 * (rho >> 3) + (rho & 3); }
 
-__device__ __forceinline__ h8 buffer_load16(__amdgpu_buffer_rsrc_t r, int voff, int soff)
-{
-    return __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
-}
-
-// One operand tile of R rows (output rows of A, or output columns of B) by
-// 64 reduction indices: the staging registers and the global -> register and
-// register -> LDS copies.  The tile origin is always inside the matrix and
-// the tile never extends past its last row (edge tiles are shifted back), so
-// every chunk address is one per-lane offset plus a per-chunk scalar offset.
-// Only reduction indices at or beyond K must read as zero: the per-lane
-// offset of such a chunk is replaced by OOB_OFFSET.
-//   KCONT: reduction-contiguous in global memory (row-major A, col-major B):
-//          lane t copies chunk t%8 of rows t/8 + (NT/8)*p.
-//   otherwise: lane t copies the 8 x 8 block (reduction rows 8*kb..8*kb+7,
-//          tile rows 8*rb..8*rb+7), rb = idx % (R/8), kb = idx / (R/8),
-//          idx = t + NT*p, and transposes it in registers.
-template <int R, int NT, bool KCONT>
-struct FastStage {
-    static constexpr int RB = R / 8;                    // 8-row groups of the tile
-    static constexpr int PER = KCONT ? R * 8 / NT : (R + NT - 1) / NT;
-    static constexpr int NREG = KCONT ? PER : PER * 8;
-    static constexpr bool PARTIAL = !KCONT && R % NT != 0;  // some lanes idle
-    static_assert(!KCONT || (R * 8) % NT == 0, "chunks must divide evenly among the threads");
-    static_assert(KCONT || NT % RB == 0 || R < NT, "blocks must tile the threads");
-
-    int voff;        // byte offset of the lane's first chunk from the step origin
-    int lds0;        // KCONT: LDS byte offset of the lane's first chunk
-    int ldsr[KCONT ? 1 : PER * 8];  // transposing: LDS byte offset of each written row
-    int kq;          // reduction offset (elements) of the lane's first chunk
-    bool live;       // transposing: this lane owns a block
-    int64_t ldb2;    // leading dimension in bytes
-    h8 v[NREG];
-
-    __device__ __forceinline__ void init(int64_t ld, int tid)
-    {
-        ldb2 = ld * 2;
-        if constexpr (KCONT) {
-            const int r = tid >> 3, c = tid & 7;
-            voff = (int)(r * ldb2) + 16 * c;
-            lds0 = (r * 8 + (c ^ swz32(r))) * 16;
-            kq = 8 * c;
-            live = true;
-        } else {
-            const int rb = tid % RB, kb = tid / RB;
-            live = tid < R;
-            voff = (int)(8 * kb * ldb2) + 16 * rb;
-            kq = 8 * kb;
-#pragma unroll
-            for (int p = 0; p < PER; ++p)
-#pragma unroll
-                for (int rr = 0; rr < 8; ++rr) {
-                    const int r = 8 * rb + rr;
-                    ldsr[p * 8 + rr] = (r * 8 + ((kb + p * (NT / RB)) ^ swz32(r))) * 16;
-                }
-        }
-    }
-
-    // Scalar byte offset of staging register i.
-    __device__ __forceinline__ int soff(int i) const
-    {
-        if constexpr (KCONT) return (int)(i * (NT / 8) * ldb2);
-        else return (int)(((i / 8) * (NT / RB) * 8 + (i % 8)) * ldb2);
-    }
-    // Reduction index (relative to the step) of staging register i's chunk.
-    __device__ __forceinline__ int kidx(int i) const
-    {
-        if constexpr (KCONT) return kq;
-        else return kq + (i / 8) * (NT / RB) * 8 + (i % 8);
-    }
-
-    // Loads of one step; chunks at or beyond kleft (= K - step origin) read
-    // as zero.
-    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, int kleft)
-    {
-#pragma unroll
-        for (int i = 0; i < NREG; ++i) v[i] = buffer_load16(rs, kidx(i) < kleft ? voff : OOB_OFFSET, soff(i));
-    }
-
-    __device__ __forceinline__ void store(char *lds) const
-    {
-        if constexpr (KCONT) {
-#pragma unroll
-            for (int p = 0; p < PER; ++p)
-                *reinterpret_cast<h8 *>(lds + lds0 + p * (NT / 8) * 128) = v[p];
-        } else {
-#pragma unroll
-            for (int p = 0; p < PER; ++p) {
-                if (!PARTIAL || live) {
-#pragma unroll
-                    for (int rr = 0; rr < 8; ++rr) {
-                        h8 t;
-#pragma unroll
-                        for (int q = 0; q < 8; ++q) t[q] = v[p * 8 + q][rr];
-                        *reinterpret_cast<h8 *>(lds + ldsr[p * 8 + rr]) = t;
-                    }
-                }
-            }
-        }
-    }
-};
-
 typedef __attribute__((address_space(3))) void lds_void;
 
 // s_waitcnt vmcnt(VM) lgkmcnt(0): all but the VM most recent global loads
@@ -205,8 +105,8 @@ __device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t rs, cha
 // Scheduling hints for one 16-deep slice of NM MFMAs: the NR fragment reads
 // for the next slice go first (so they have the whole slice to land), then
 // the MFMAs, each followed by its share of the CNT instructions of class
-// MASK (staging writes 0x200 or global copies 0x020), so those are spread
-// evenly over the slice instead of queueing behind each other.
+// MASK (global copies: 0x020), so those are spread evenly over the slice
+// instead of queueing behind each other.
 template <int NM, int NR, int MASK, int CNT, int I = 0>
 __device__ __forceinline__ void sched_slice()
 {
@@ -218,30 +118,6 @@ __device__ __forceinline__ void sched_slice()
         sched_slice<NM, NR, MASK, CNT, I + 1>();
     }
 }
-
-// Register-staged copy of one operand tile (any layout): global -> registers
-// during one step, registers -> LDS during the next.  RELU: the prologue's
-// ReLU is applied to the staged values between the two copies, so LDS holds
-// relu(X) and the footprint is that of the plain operand (Pointwise
-// Operations in Prologue subsection).
-template <int R, int NT, bool KCONT, bool RELU>
-struct RegCopy {
-    using Stage = FastStage<R, NT, KCONT>;
-    static constexpr int NLOAD = Stage::NREG;                   // global loads per step
-    static constexpr int NWRITE = KCONT ? Stage::PER : Stage::PER * 8;  // LDS writes per step
-    Stage st;
-    __device__ __forceinline__ void init(int64_t ld, int tid) { st.init(ld, tid); }
-    __device__ __forceinline__ void dma(__amdgpu_buffer_rsrc_t, char *, int) {}
-    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, int kleft) { st.load(rs, kleft); }
-    __device__ __forceinline__ void write(char *stage)
-    {
-        if constexpr (RELU) {
-#pragma unroll
-            for (int i = 0; i < Stage::NREG; ++i) st.v[i] = relu_h8(st.v[i]);
-        }
-        st.store(stage);
-    }
-};
 
 // Direct global -> LDS copy of a reduction-contiguous operand tile with the
 // gfx950 buffer_load_dwordx4 ... lds form: each instruction moves 64 chunks
@@ -258,7 +134,6 @@ struct DmaCopy {
     static constexpr int NV0 = (8 * NW) % 32 == 0 ? 1 : 32 / (8 * NW);
     static constexpr int NV = NV0 < NI ? NV0 : NI;            // distinct lane offsets
     static constexpr int NLOAD = NI;
-    static constexpr int NWRITE = 0;
     static_assert(R % (8 * NW) == 0, "rows must divide evenly among the waves");
 
     int voff[NV];  // lane byte offset from the instruction's first row
@@ -292,8 +167,6 @@ struct DmaCopy {
                               (int)(row0 * ldb2));
         }
     }
-    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t, int) {}
-    __device__ __forceinline__ void write(char *) {}
 };
 
 // LDS layout of an operand tile that is contiguous along M (column-major A)
@@ -322,7 +195,6 @@ struct DmaCopyT {
     static constexpr int RPI = 1024 / (2 * R);    // rows per instruction
     static constexpr int NI = 64 / (RPI * NW);    // instructions per wave per step
     static constexpr int NLOAD = NI;
-    static constexpr int NWRITE = 0;
     static_assert(R >= 32 && R <= 512 && (R & (R - 1)) == 0, "rows of 32 to 512 elements");
     static_assert(64 % (RPI * NW) == 0, "rows must divide evenly among the waves");
 
@@ -354,8 +226,6 @@ struct DmaCopyT {
                               (int)(g * RPI * ldb2));
         }
     }
-    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t, int) {}
-    __device__ __forceinline__ void write(char *) {}
 };
 
 // Lane byte offset, inside such a tile, of the first transposing read of the
@@ -393,15 +263,12 @@ __device__ __forceinline__ h8 read_frag_tr(const char *p)
 // 64-deep slab of the reduction (SK slabs per step, each in its own LDS
 // sub-stage), and after the last step the SK partial tiles are summed
 // through LDS before the epilogue.
-// NSTG (a power of two) LDS stages are used when both operands are copied
-// directly into LDS: the copies of a step are then issued NSTG - 1 steps
-// before the step is multiplied, so small tiles that cannot cover the
-// memory latency with work hide it with depth.  Register-staged operands
-// keep two stages.
+// NSTG (a power of two) LDS stages: the copies of a step are issued
+// NSTG - 1 steps before the step is multiplied, so small tiles that cannot
+// cover the memory latency with work hide it with depth.
 // PRO: the prologue's ReLU on the left operand of every product (Pointwise
-// Operations in Prologue subsection): applied to the staged registers when
-// that operand is register-staged, else to its MFMA fragments as they leave
-// LDS; either way LDS holds one copy of the operand.
+// Operations in Prologue subsection), applied to its MFMA fragments as they
+// leave LDS, so LDS holds one copy of the operand.
 // DUAL: a second product P.Q of the same output shape is accumulated into
 // the same registers after A.B (Matmuls with Pointwise Epilogue
 // subsection): the reduction runs over A.B's K steps and then over P.Q's K2
@@ -410,8 +277,8 @@ __device__ __forceinline__ h8 read_frag_tr(const char *p)
 // (the grid holds p.splits workgroups per tile); every split writes its
 // fp32 partial tile to p.ws and the last one of a tile to arrive sums them
 // in split order and runs the epilogue.
-template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool DMA,
-          bool PRO, bool DUAL, bool SPLIT>
+template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool PRO, bool DUAL,
+          bool SPLIT>
 __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs p)
 {
     constexpr int NTG = 64 * WM * WN;         // threads per k-group
@@ -423,13 +290,9 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
     constexpr int SUB = (BM + BN) * ROWB;     // bytes per k-group sub-stage
     constexpr int STAGE = SK * SUB;           // bytes per LDS stage
     // Operands contiguous along the reduction use DmaCopy and ds_read_b128
-    // fragments, the others DmaCopyT and transposing reads (TA / TB); with
-    // DMA false the latter are register-staged and transposed before the
-    // LDS write instead.
-    constexpr bool TA = DMA && LA == COL, TB = DMA && LB == ROW;
-    constexpr bool DMA_A = DMA, DMA_B = DMA;  // copied straight into LDS
-    constexpr bool DEEP = DMA_A && DMA_B;
-    constexpr int NS = DEEP ? NSTG : 2;       // LDS stages
+    // fragments, the others (TA / TB) DmaCopyT and transposing reads.
+    constexpr bool TA = LA == COL, TB = LB == ROW;
+    constexpr int NS = NSTG;                  // LDS stages
     static_assert((NS & (NS - 1)) == 0, "stage count must be a power of two");
     constexpr int PADN = BN + 4;              // fp32 row pitch of the split-K partial tiles
     constexpr int RED = SK > 1 ? SK * BM * PADN * 4 : 0;
@@ -466,11 +329,8 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
     const int mc = m0 + BM <= p.M ? m0 : p.M - BM;
     const int nc = n0 + BN <= p.N ? n0 : p.N - BN;
 
-    constexpr bool FRAG_RELU = PRO && DMA_A;  // ReLU on fragments (no register stage)
-    using CopyA = std::conditional_t<
-        DMA_A, std::conditional_t<TA, DmaCopyT<BM, NTG>, DmaCopy<BM, NTG>>, RegCopy<BM, NTG, LA == ROW, PRO>>;
-    using CopyB = std::conditional_t<
-        DMA_B, std::conditional_t<TB, DmaCopyT<BN, NTG>, DmaCopy<BN, NTG>>, RegCopy<BN, NTG, LB == COL, false>>;
+    using CopyA = std::conditional_t<TA, DmaCopyT<BM, NTG>, DmaCopy<BM, NTG>>;
+    using CopyB = std::conditional_t<TB, DmaCopyT<BN, NTG>, DmaCopy<BN, NTG>>;
     CopyA ca;
     CopyB cb;
 
@@ -521,7 +381,7 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
         }
     };
     auto mfmas = [&](int buf) {
-        if constexpr (FRAG_RELU) {
+        if constexpr (PRO) {
             // the prologue's ReLU, once per fragment, right before its use
             // (so the fragment read in flight is not waited for early)
 #pragma unroll
@@ -553,11 +413,10 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
     };
 
     // Instruction interleaving hints for the scheduler: each MFMA is paired
-    // with the fragment read (DS read), staging write (DS write) or global
-    // load (VMEM read) that has to overlap it.
+    // with the fragment read (DS read) or global copy (VMEM read) that has
+    // to overlap it.
     constexpr int NM = TN * TM;           // MFMAs per 16-deep slice
     constexpr int NR = TM * (TA ? 2 : 1) + TN * (TB ? 2 : 1);  // fragment reads per slice
-    constexpr int NW = CopyA::NWRITE + CopyB::NWRITE;
     constexpr int NL = CopyA::NLOAD + CopyB::NLOAD;
     // Global loads still allowed in flight at the barrier of step kt: the
     // copies of steps kt+2 .. kt+NS-1; step kt+1 must have landed.
@@ -606,11 +465,10 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
         }
         const int nk = s_hi - s_lo;
 
-        // Copies of step s (this k-group's slab): direct-to-LDS operands into
-        // `stage`, the others into their staging registers.  Steps past the
-        // last one re-fetch the last step (into a stage nobody reads again), so
-        // every step of the loop below has the same shape.  A slab starting at
-        // or beyond K reads as zeros.
+        // Copies of step s (this k-group's slab) into `stage`.  Steps past
+        // the last one re-fetch the last step (into a stage nobody reads
+        // again), so every step of the loop below has the same shape.  A slab
+        // starting at or beyond K reads as zeros.
         auto copy_step = [&](int s, char *stage) {
             // wave-uniform; without readfirstlane the compiler may take it
             // (through the k-group index, from the thread index, or the
@@ -622,26 +480,21 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
             const auto rb = rsrc_b(k0);
             ca.dma(ra, stage, kleft);
             cb.dma(rb, stage + BM * ROWB, kleft);
-            ca.load(ra, kleft);
-            cb.load(rb, kleft);
         };
 
-        // Prologue: step 0 into LDS stage 0 and step 1 under way (into stage 1
-        // or the staging registers), then the first fragments of step 0.
+        // Prologue: steps 0 .. NS-1 into the LDS stages, then the first
+        // fragments of step 0.
         if (nk > 0) {
-            copy_step(0, mine);
-            ca.write(mine);
-            cb.write(mine + BM * ROWB);
 #pragma unroll
-            for (int s = 1; s < NS; ++s) copy_step(s, mine + s * STAGE);
+            for (int s = 0; s < NS; ++s) copy_step(s, mine + s * STAGE);
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             read_frags(0, mine, 0);
         }
 
-        // One reduction step.  On entry LDS stage `cur` holds step kt, step kt+1
-        // is under way (into `nxt` or the staging registers) and fq/fp[0] hold
-        // slice 0 of step kt.
+        // One reduction step.  On entry LDS stage `cur` holds step kt, steps
+        // kt+1 .. kt+NS-1 are under way into the other stages and fq/fp[0]
+        // hold slice 0 of step kt.
         for (int kt = 0; kt < nk; ++kt) {
             char *cur = mine + (kt & (NS - 1)) * STAGE;
             char *nxt = mine + ((kt + 1) & (NS - 1)) * STAGE;
@@ -654,12 +507,10 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
             mfmas(1);
             round16();
             sched_slice<NM, NR, 0, 0>();
-            // slice 2, plus the register-staged writes of step kt+1
+            // slice 2
             read_frags(1, cur, 3);
             mfmas(0);
-            ca.write(nxt);
-            cb.write(nxt + BM * ROWB);
-            sched_slice<NM, NR, 0x200, NW>();
+            sched_slice<NM, NR, 0, 0>();
             // Step kt+1 complete in LDS for every wave; every read of `cur` done.
             if constexpr (VM_AT_BARRIER == 0) {
                 __builtin_amdgcn_s_waitcnt(0);

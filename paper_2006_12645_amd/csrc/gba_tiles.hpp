@@ -24,7 +24,7 @@ struct TileCfg {
 // workgroup, WM x WN waves, each owning a (BM/WM) x (BN/WN) warp tile
 // (multiples of 32 x 32, the MFMA block), times SK k-groups of waves that
 // split each reduction step (intra-workgroup split-K; fp32 accumulation
-// only); NSTG LDS stages when both operands are copied directly into LDS.
+// only); NSTG LDS stages.
 #define GBA_TILE_LIST(X)         \
     X(0, 256, 256, 2, 2, 1, 2)   \
     X(1, 256, 256, 2, 4, 1, 2)   \
@@ -75,7 +75,7 @@ hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
 {
     // one workgroup per output tile, times the splits of its reduction
     dim3 grid((unsigned)(a.tiles_m * a.tiles_n * (SPLIT ? a.splits : 1))), block(64 * WM * WN * SK);
-    hipLaunchKernelGGL((gemm_bias_act_fast<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, true, PRO, DUAL, SPLIT>), grid,
+    hipLaunchKernelGGL((gemm_bias_act_fast<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, PRO, DUAL, SPLIT>), grid,
                        block, 0, s, a);
     return hipGetLastError();
 }
