@@ -349,6 +349,16 @@ def test_split_deterministic_and_reusable():
     U.assert_close(first, pr.oracle(), what="split 8")
 
 
+@pytest.mark.parametrize("tile", [None, 4, 6, 9])
+def test_mn_contiguous_operands_all_features_odd_k(tile):
+    # column-major A and P, row-major B and Q: fast path with K and K2 odd,
+    # prologue on the transposed fragments, difference of products, full bias
+    announce("CR all features odd K", tile)
+    pr = Problem(849, 200, 136, 333, K2=71, full_bias=True)
+    kw = dict(prologue=True, second="sub", bias_op="sub", act="sigmoid")
+    U.assert_close(pr.gpu("CR", **kw, tile=tile), pr.oracle(**kw), what=f"CR odd K tile {tile}")
+
+
 def test_split_workspace_reused_with_new_data():
     # a second problem through the same workspace reads its own partials,
     # not the first one's

@@ -189,6 +189,29 @@ def test_deep_pipeline_short_and_long_k(tile, K):
     U.assert_close(got, U.oracle_for(A, B, bias), what=f"deep tile {tile} K={K}")
 
 
+@pytest.mark.parametrize("tile", [None, 1, 4, 6, 9, 11, 13])
+@pytest.mark.parametrize("K", [1, 5, 77, 130])
+def test_mn_contiguous_operands_any_k(tile, K):
+    """Column-major A with row-major B keeps the fast path for any K (both
+    operands are contiguous along M / N): reduction rows past K in the last
+    step are zero-filled row by row."""
+    M, N = 264, 296
+    announce("CR any K", tile, K)
+    A, B, bias = D.random_problem(3500 + K, M, N, K)
+    got = run_gpu(A, B, bias, "CR", tile=tile).cpu().numpy()
+    U.assert_close(got, U.oracle_for(A, B, bias), what=f"CR tile {tile} K={K}")
+
+
+@pytest.mark.parametrize("layout", ["RR", "CR", "CC"])
+@pytest.mark.parametrize("tile", [11, 13])
+def test_deep_pipeline_transposed_layouts(layout, tile):
+    M, N, K = 136, 200, 5000
+    announce("deep", layout, tile)
+    A, B, bias = D.random_problem(3600 + tile, M, N, K)
+    got = run_gpu(A, B, bias, layout, tile=tile).cpu().numpy()
+    U.assert_close(got, U.oracle_for(A, B, bias), what=f"deep {layout} tile {tile}")
+
+
 def test_long_k_selects_split_k():
     """A long reduction over few output tiles takes the split-K tile."""
     M, N, K = 96, 320, 8192
