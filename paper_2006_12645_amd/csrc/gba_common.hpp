@@ -54,6 +54,15 @@ __device__ __forceinline__ h8 zero_h8()
     return z;
 }
 
+typedef float f2v __attribute__((ext_vector_type(2)));
+typedef _Float16 h2v __attribute__((ext_vector_type(2)));
+
+// Two fp32 values rounded to the nearest fp16 (ties to even) and back.
+__device__ __forceinline__ f2v round_f16x2(f2v x)
+{
+    return __builtin_convertvector(__builtin_convertvector(x, h2v), f2v);
+}
+
 typedef short s8 __attribute__((ext_vector_type(8)));
 
 // max(x, 0) on eight fp16 values (the ReLU of a prologue), as a signed

@@ -400,14 +400,19 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
     };
     auto round16 = [&]() {
         // fp16 accumulation: the running sum is rounded to fp16 at the end of
-        // every aligned 32-deep group of k.
+        // every aligned 32-deep group of k (pairs: one v_cvt_pk_f16_f32 and
+        // two v_cvt_f32_f16 per two values, against four single conversions).
         if constexpr (ACC16) {
 #pragma unroll
             for (int t = 0; t < TN; ++t)
 #pragma unroll
                 for (int s = 0; s < TM; ++s)
 #pragma unroll
-                    for (int e = 0; e < 16; ++e) acc[t][s][e] = (float)(_Float16)acc[t][s][e];
+                    for (int e = 0; e < 16; e += 2) {
+                        const f2v r = round_f16x2(f2v{acc[t][s][e], acc[t][s][e + 1]});
+                        acc[t][s][e] = r[0];
+                        acc[t][s][e + 1] = r[1];
+                    }
         }
     };
     auto negate_acc = [&]() {

@@ -267,7 +267,11 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_generic(GemmArgs p
 #pragma unroll
                         for (int s = 0; s < TM; ++s)
 #pragma unroll
-                            for (int e = 0; e < 4; ++e) acc[t][s][e] = (float)(_Float16)acc[t][s][e];
+                            for (int e = 0; e < 4; e += 2) {
+                                const f2v r = round_f16x2(f2v{acc[t][s][e], acc[t][s][e + 1]});
+                                acc[t][s][e] = r[0];
+                                acc[t][s][e + 1] = r[1];
+                            }
                 }
             }
             if (more) {
