@@ -1,0 +1,92 @@
+"""Randomised requests through gba_fused_gemm against the oracle: every
+combination of layout, tile (or the library's choice), prologue, second
+product, bias kind and sign, activation, accumulation, reduction split and
+operand alignment, on seeded random shapes that mostly are not multiples of
+the tiles.  Each case prints its parameters before touching the GPU.
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2006_12645_amd import datagen as D
+from paper_2006_12645_amd import gba
+
+import gpu_util as U
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+ACT = {"none": O.ACT_NONE, "relu": O.ACT_RELU, "sigmoid": O.ACT_SIGMOID, "tanh": O.ACT_TANH}
+NUM_CASES = 64
+
+
+def draw(seed):
+    """One random request (plain Python values)."""
+    rng = np.random.default_rng(90000 + seed)
+    pick = lambda xs: xs[int(rng.integers(len(xs)))]
+    # sizes: mostly multiples of 8 (fast path), sometimes not
+    mult = 8 if rng.random() < 0.75 else 1
+    M = int(rng.integers(1, 50)) * mult + (0 if mult == 8 else int(rng.integers(1, 8)))
+    N = int(rng.integers(1, 50)) * mult + (0 if mult == 8 else int(rng.integers(1, 8)))
+    K = int(rng.integers(0, 90)) * 8 + (int(rng.integers(0, 8)) if rng.random() < 0.3 else 0)
+    c = dict(M=M, N=N, K=K, layout=pick(["RR", "RC", "CR", "CC"]),
+             prologue=bool(rng.random() < 0.5), act=pick(list(ACT)),
+             accum="f16" if rng.random() < 0.25 else "f32",
+             bias=pick([None, "row", "full"]), bias_op=pick(["add", "sub"]),
+             second=pick([None, "add", "sub"]), K2=int(rng.integers(0, 60)) * 8,
+             offset=bool(rng.random() < 0.1), tile=None, split=None)
+    tiles = [t for t in range(gba.num_tiles())
+             if gba.tile_info(t)["bm"] <= M and gba.tile_info(t)["bn"] <= N]
+    if tiles and rng.random() < 0.6:
+        c["tile"] = pick(tiles)
+    if c["accum"] == "f32" and rng.random() < 0.3:
+        c["split"] = int(rng.integers(2, 9))
+    return c
+
+
+def operand(x, lay, offset):
+    """Device tensor of logical matrix x stored in layout lay (leading
+    dimension padded by 8); offset: storage shifted by one element."""
+    rows, cols = x.shape
+    ext = (cols if lay == D.ROW else rows) + 8
+    st = D.store(x, lay, ext)
+    flat = torch.empty(st.size + 1, dtype=torch.float16, device="cuda")
+    t = (flat[1:] if offset else flat[:-1]).view(st.shape)
+    t.copy_(torch.from_numpy(st).cuda())
+    return t[:, :cols] if lay == D.ROW else t[:, :rows].t()
+
+
+@pytest.mark.parametrize("seed", range(NUM_CASES))
+def test_random_request(seed):
+    c = draw(seed)
+    print("CASE", seed, c, flush=True)
+    M, N, K = c["M"], c["N"], c["K"]
+    A, B, _ = D.random_problem(91000 + seed, M, N, K)
+    K2 = c["K2"]
+    P = Q = None
+    if c["second"]:
+        P, Q, _ = D.random_problem(92000 + seed, M, N, K2)
+    bias = None
+    if c["bias"] == "row":
+        bias = D.uniform_f16(93000 + seed, (N,))
+    elif c["bias"] == "full":
+        bias = D.uniform_f16(93000 + seed, (M, N))
+    la, lb = D.LAYOUT_NAMES[c["layout"]]
+    dev = lambda x, lay: None if x is None else operand(x, lay, c["offset"])
+    dbias = None
+    if bias is not None:
+        dbias = torch.from_numpy(bias).cuda() if bias.ndim == 1 else operand(bias, D.ROW, c["offset"])
+    got = gba.fused_gemm(dev(A, la), dev(B, lb), P=dev(P, la), Q=dev(Q, lb), second=c["second"] or "add",
+                         prologue="relu" if c["prologue"] else None, bias=dbias, bias_op=c["bias_op"],
+                         act=c["act"], accum=c["accum"], tile=c["tile"], split=c["split"])
+    torch.cuda.synchronize()
+    sec = 0 if P is None else (1 if c["second"] == "add" else -1)
+    ref = O.fused(D.store(A, D.ROW), D.ROW, D.store(B, D.COL), D.COL, M, N, K,
+                  prologue_relu=c["prologue"], second=sec,
+                  p_store=None if P is None else D.store(P, D.ROW),
+                  q_store=None if Q is None else D.store(Q, D.COL), K2=K2 if P is not None else 0,
+                  bias=bias, bias_kind=(O.BIAS_NONE if bias is None else
+                                        O.BIAS_ROW if bias.ndim == 1 else O.BIAS_FULL),
+                  bias_sign=1 if c["bias_op"] == "add" else -1, act=ACT[c["act"]],
+                  acc16=c["accum"] == "f16")
+    U.assert_close(got.cpu().numpy(), ref, accum=c["accum"], what=f"case {seed}")
