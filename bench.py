@@ -17,6 +17,7 @@ and a ReLU); their metric counts 2MN(K + K2) flops.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--tile ID]
                     [--report PATH] [--no-cpu]
+    python bench.py --configs      # every workload configuration, one line each
 """
 import argparse
 import hashlib
@@ -105,6 +106,41 @@ def cpu_baseline(w, A, B, bias, P=None, Q=None, target_s=12.0):
                       f"fp64, {dt:.1f} s"}
 
 
+def configs(args, np, torch, D, gba):
+    """Every single-product workload configuration: layouts x accumulations,
+    the library's tile choice, fused launches timed like the headline.  The
+    roofline bound is HBM below the ridge point (peak flops / peak bytes)
+    and MFMA above it."""
+    ridge = PEAK_F16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    for w in D.WORKLOADS.values():
+        if w.extra:
+            continue
+        A, B, bias = D.logical_inputs(w)
+        dbias = torch.from_numpy(bias).cuda()
+        out = torch.empty((w.M, w.N), dtype=torch.float16, device="cuda")
+        for layout in w.layouts:
+            la, lb = D.LAYOUT_NAMES[layout]
+            dA = (torch.from_numpy(A).cuda() if la == D.ROW
+                  else torch.from_numpy(np.ascontiguousarray(A.T)).cuda().t())
+            dB = (torch.from_numpy(B).cuda() if lb == D.ROW
+                  else torch.from_numpy(np.ascontiguousarray(B.T)).cuda().t())
+            for acc in w.accum:
+                fn = lambda: gba.gemm_bias_act(dA, dB, dbias, act="relu", accum=acc, out=out)
+                ms = time_launches(fn, args.steps, args.warmup, torch)
+                flops = 2.0 * w.M * w.N * w.K
+                nbytes = 2.0 * (w.M * w.K + w.K * w.N + w.M * w.N + w.N)
+                tf = flops / (ms * 1e-3) / 1e12
+                gbs = nbytes / (ms * 1e-3) / 1e9
+                hbm = flops / nbytes < ridge
+                print(json.dumps({
+                    "workload": w.name, "M": w.M, "N": w.N, "K": w.K, "layout": layout, "accum": acc,
+                    "tile": gba.select_tile(w.M, w.N, w.K, la, lb, acc), "us": round(ms * 1e3, 2),
+                    "TFLOP/s": round(tf, 1), "GB/s": round(gbs, 1),
+                    "roofline": {"bound": "hbm" if hbm else "mfma",
+                                 "frac": round(gbs / PEAK_HBM_GBS if hbm else tf / PEAK_F16_TFLOPS, 4)},
+                }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -119,6 +155,10 @@ def main():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device-to-device copies of MIB MiB (the reference "
                          "kernel for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE) and exit")
+    ap.add_argument("--configs", action="store_true",
+                    help="instead of the headline line: one JSON line per workload "
+                         "configuration (every layout and accumulation it lists) with its "
+                         "roofline position")
     args = ap.parse_args()
 
     if args.calibrate_copy:
@@ -144,6 +184,9 @@ def main():
     from paper_2006_12645_amd import gba
 
     gba.lib()  # raises if the HIP library is not built
+    if args.configs:
+        configs(args, np, torch, D, gba)
+        return
     w = D.WORKLOADS[args.workload]
     A, B, bias = D.logical_inputs(w)
     dA = torch.from_numpy(A).cuda()                                    # row-major
