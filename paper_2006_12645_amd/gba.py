@@ -89,9 +89,16 @@ def _check(status, what):
 
 
 def _stream_handle(stream, device):
+    """The HIP stream to launch on: `stream`, else torch's current stream of
+    `device` (read through torch's raw-pointer accessor when it has one,
+    which costs ~0.1 us against ~2 us for a Stream object)."""
     import torch
     if stream is None:
-        stream = torch.cuda.current_stream(device)
+        raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+        dev = torch.device(device) if device is not None else torch.device("cuda")
+        if raw is not None:
+            return ctypes.c_void_p(raw(dev.index if dev.index is not None else torch.cuda.current_device()))
+        stream = torch.cuda.current_stream(dev)
     return ctypes.c_void_p(stream.cuda_stream)
 
 
