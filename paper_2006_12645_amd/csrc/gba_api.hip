@@ -71,7 +71,9 @@ bool tile_fits(int tile, int64_t M, int64_t N) { return M >= TILES[tile].bm && N
 //     from 400;
 //   * a reduction of 1024 or more (fp32 accumulation only) whose 64x64
 //     tiles fit in one round of 160 (from K = 2048: 88) to 256 workgroups
-//     takes 64x64 with two k-groups of waves (intra-workgroup split-K);
+//     takes 64x64 with two k-groups of waves (intra-workgroup split-K) --
+//     below 128 of them, 32x64 with four k-groups if that makes at most
+//     256;
 //     from K = 2048, with fewer
 //     output tiles still, 64x64 with two k-groups while that makes more
 //     than 64 workgroups, else 32x32 with four k-groups and four LDS
@@ -94,7 +96,8 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum)
     if (tiles(t57) >= 400) return t57;
     if (accum == GBA_ACC_F32 && K >= 1024) {
         const int64_t n11 = tiles(11), n8 = tiles(8);
-        if (n11 >= (K >= 2048 ? 88 : 160) && n11 <= 256) return 11;
+        if (n11 >= (K >= 2048 ? 88 : 160) && n11 <= 256)
+            return n11 < 128 && tiles(12) <= 256 ? 12 : 11;
         if (K >= 2048 && (n8 < 128 || (K >= 4096 && n8 <= 128))) {
             if (n11 > 64) return 11;
             if (tile_fits(13, M, N)) return 13;
