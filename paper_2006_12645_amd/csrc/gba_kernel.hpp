@@ -476,16 +476,17 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
         const int nk = s_hi - s_lo;
 
         // Copies of step s (this k-group's slab) into `stage`.  Steps past
-        // the last one re-fetch the last step (into a stage nobody reads
-        // again), so every step of the loop below has the same shape.  A slab
-        // starting at or beyond K reads as zeros.
+        // the last one are issued too, so every step of the loop below has
+        // the same shape, but entirely with out-of-range offsets: they write
+        // zeros into a stage nobody reads again without touching memory.  A
+        // slab starting at or beyond K reads as zeros.
         auto copy_step = [&](int s, char *stage) {
             // wave-uniform; without readfirstlane the compiler may take it
             // (through the k-group index, from the thread index, or the
             // split range) for divergent and loop over the lanes of every
             // copy
             const int k0 = __builtin_amdgcn_readfirstlane((((s < nk ? s : nk - 1) + s_lo) * SK + grp) * BK);
-            const int kleft = Kseg - k0;
+            const int kleft = s < nk ? Kseg - k0 : 0;
             const auto ra = rsrc_a(k0);
             const auto rb = rsrc_b(k0);
             ca.dma(ra, stage, kleft);
