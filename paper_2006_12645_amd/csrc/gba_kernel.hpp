@@ -433,6 +433,21 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
     constexpr int VM_AT_BARRIER = (NS - 2) * NL;
     char *const mine = lds + grp * SUB;   // this k-group's sub-stage of stage 0
 
+    // The row bias of this lane's output columns, loaded before the
+    // reduction so its latency is hidden behind it (the epilogue of the
+    // single k-group tiles uses it from registers).
+    h8 brow[SK == 1 ? TN : 1][2];
+    if constexpr (SK == 1) {
+        if (p.bias_kind == BIAS_ROW) {
+#pragma unroll
+            for (int t = 0; t < TN; ++t) {
+                const _Float16 *bp = p.bias + nc + wn * WTN + 32 * t + 16 * hi;
+                brow[t][0] = *reinterpret_cast<const h8 *>(bp);
+                brow[t][1] = *reinterpret_cast<const h8 *>(bp + 8);
+            }
+        }
+    }
+
     // One pass of the pipelined reduction per product: A.B, then (DUAL)
     // P.Q on top of it.  C - R is formed as -((-C) + R): negating the
     // running sum is exact and rounding is symmetric, so this equals
@@ -498,8 +513,12 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
         if (nk > 0) {
 #pragma unroll
             for (int s = 0; s < NS; ++s) copy_step(s, mine + s * STAGE);
-            __builtin_amdgcn_s_waitcnt(0);
-            __syncthreads();
+            // step 0 landed for every wave (the later steps may still be in
+            // flight: the loop's barriers wait for them)
+            __builtin_amdgcn_sched_barrier(0);
+            wait_vm_lgkm0<(NS - 1) * NL>();
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
             read_frags(0, mine, 0);
         }
 
@@ -668,14 +687,11 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
     float b[TN][16];
 #pragma unroll
     for (int t = 0; t < TN; ++t) {
-        const int j = nc + wn * WTN + 32 * t + 16 * hi;
         if (p.bias_kind == BIAS_ROW) {
-            const h8 b0 = *reinterpret_cast<const h8 *>(p.bias + j);
-            const h8 b1 = *reinterpret_cast<const h8 *>(p.bias + j + 8);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                b[t][e] = p.bias_sign * (float)b0[e];
-                b[t][8 + e] = p.bias_sign * (float)b1[e];
+                b[t][e] = p.bias_sign * (float)brow[t][0][e];
+                b[t][8 + e] = p.bias_sign * (float)brow[t][1][e];
             }
         } else {
 #pragma unroll
