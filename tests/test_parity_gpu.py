@@ -353,6 +353,47 @@ def test_deterministic_and_stream():
     assert torch.equal(a, c)
 
 
+def test_graph_capture_replays():
+    """The fused kernels captured in a HIP graph (a plain call, a call with
+    the reduction split across workgroups through a caller workspace, and
+    the transposed layout) replay to the eager results, replay after replay,
+    with eager work of the library on the same buffers in between."""
+    announce("graph capture")
+    M, N, K = 384, 256, 4096
+    A, B, bias = D.random_problem(69, M, N, K)
+    dA, dB = U.device_operand(A, D.ROW), U.device_operand(B, D.COL)
+    dAc, dBr = U.device_operand(A, D.COL), U.device_operand(B, D.ROW)
+    dbias = torch.from_numpy(bias).cuda()
+    ws = torch.zeros(16 << 20, dtype=torch.uint8, device="cuda")
+    outs = [torch.empty(M, N, dtype=torch.float16, device="cuda") for _ in range(3)]
+    calls = [lambda: gba.gemm_bias_act(dA, dB, dbias, out=outs[0]),
+             lambda: gba.fused_gemm(dA, dB, bias=dbias, tile=6, split=8, workspace=ws, out=outs[1]),
+             lambda: gba.fused_gemm(dAc, dBr, bias=dbias, act="tanh", out=outs[2])]
+    for f in calls:
+        f()
+    torch.cuda.synchronize()
+    eager = [o.clone() for o in outs]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for f in calls:
+            f()
+    torch.cuda.synchronize()
+    for rep in range(4):
+        for o in outs:
+            o.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        for o, e in zip(outs, eager):
+            assert torch.equal(o, e), f"replay {rep}"
+        # eager work in between, on the same workspace and outputs
+        calls[1]()
+        calls[0]()
+        torch.cuda.synchronize()
+    assert not ws[:(M // 64) * (N // 64) * 4].any().item()  # the split's counters are back at 0
+
+
 def test_unfused_pieces():
     M, N = 333, 1031
     announce("pointwise")
