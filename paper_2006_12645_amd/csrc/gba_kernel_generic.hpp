@@ -65,11 +65,15 @@ __device__ __forceinline__ int jperm(int t, int rho)
     return 32 * (t >> 1) + 8 * (rho >> 2) + 4 * (t & 1) + (rho & 3);
 }
 
+// Eight fp16 at any 2-byte alignment: gfx950 (with the unaligned access
+// mode of its HSA runtime) serves a misaligned 16-byte load or store as one
+// instruction, so these compile to single dwordx4 accesses.
+typedef _Float16 h8u __attribute__((ext_vector_type(8), aligned(2)));
+
 // Eight consecutive fp16 from p[0..7], the ones at index >= lim read as 0.
-template <bool VEC>
 __device__ __forceinline__ h8 load8(const _Float16 *p, int lim)
 {
-    if (VEC && lim >= 8) return *reinterpret_cast<const h8 *>(p);
+    if (lim >= 8) return *reinterpret_cast<const h8u *>(p);
     h8 v;
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] = e < lim ? p[e] : (_Float16)0.0f;
@@ -83,7 +87,7 @@ __device__ __forceinline__ h8 load8(const _Float16 *p, int lim)
 //         the registers to LDS (Pointwise Operations in Prologue subsection).
 // X points at the operand, ld is its leading dimension, r0/k0 the tile origin,
 // rtot/ktot the extents.
-template <int R, int BK, int NT, bool KCONT, bool VEC, bool RELU>
+template <int R, int BK, int NT, bool KCONT, bool RELU>
 struct TileCopy16 {
     static constexpr int CHUNKS = R * BK / 8;                 // 16-byte chunks per tile
     static constexpr int KCH = BK / 8;                        // chunks per LDS row
@@ -103,7 +107,7 @@ struct TileCopy16 {
                 int gr = r0 + r, gk = k0 + 8 * c;
                 h8 x = zero_h8();
                 if ((CHUNKS % NT == 0 || idx < CHUNKS) && gr < rtot && gk < ktot)
-                    x = load8<VEC>(X + (int64_t)gr * ld + gk, ktot - gk);
+                    x = load8(X + (int64_t)gr * ld + gk, ktot - gk);
                 v[p] = x;
             }
         } else {
@@ -118,7 +122,7 @@ struct TileCopy16 {
                 for (int q = 0; q < 8; ++q) {
                     h8 x = zero_h8();
                     if (live && gk0 + q < ktot && gr < rtot)
-                        x = load8<VEC>(X + (int64_t)(gk0 + q) * ld + gr, rtot - gr);
+                        x = load8(X + (int64_t)(gk0 + q) * ld + gr, rtot - gr);
                     v[p * 8 + q] = x;
                 }
             }
@@ -164,7 +168,7 @@ struct TileCopy16 {
 // PRO: ReLU prologue on the left operand of every product.  DUAL: a second
 // product P.Q is accumulated into the same registers after A.B (Matmuls
 // with Pointwise Epilogue subsection); C - R is formed as -((-C) + R).
-template <int BM, int BN, int WM, int WN, int LA, int LB, bool ACC16, bool VEC, bool PRO, bool DUAL>
+template <int BM, int BN, int WM, int WN, int LA, int LB, bool ACC16, bool PRO, bool DUAL>
 __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_generic(GemmArgs p)
 {
     constexpr int NT = 64 * WM * WN;
@@ -186,8 +190,8 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_generic(GemmArgs p
     tile_coords(blockIdx.x, gridDim.x, p.tiles_m, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
 
-    TileCopy16<BM, BK, NT, LA == ROW, VEC, PRO> ca;
-    TileCopy16<BN, BK, NT, LB == COL, VEC, false> cb;
+    TileCopy16<BM, BK, NT, LA == ROW, PRO> ca;
+    TileCopy16<BN, BK, NT, LB == COL, false> cb;
 
     f4 acc[TN][TM];
 #pragma unroll
@@ -291,7 +295,7 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_generic(GemmArgs p
         float b[8];
         if (p.bias_kind == BIAS_ROW) {
             h8 bv = zero_h8();
-            if (j < p.N) bv = load8<VEC>(p.bias + j, p.N - j);
+            if (j < p.N) bv = load8(p.bias + j, p.N - j);
 #pragma unroll
             for (int e = 0; e < 8; ++e) b[e] = p.bias_sign * (float)bv[e];
         } else {
@@ -306,7 +310,7 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_generic(GemmArgs p
             for (int e = 0; e < 8; ++e) x[e] = (e < 4 ? acc[2 * pr][s][e] : acc[2 * pr + 1][s][e - 4]) + b[e];
             if (p.bias_kind == BIAS_FULL) {
                 h8 bv = zero_h8();
-                if (i < p.M && j < p.N) bv = load8<VEC>(p.bias + (int64_t)i * p.ldbias + j, p.N - j);
+                if (i < p.M && j < p.N) bv = load8(p.bias + (int64_t)i * p.ldbias + j, p.N - j);
 #pragma unroll
                 for (int e = 0; e < 8; ++e) x[e] += p.bias_sign * (float)bv[e];
             }
@@ -316,8 +320,8 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_bias_act_generic(GemmArgs p
             for (int e = 0; e < 8; ++e) o[e] = (_Float16)x[e];
             if (i < p.M && j < p.N) {
                 _Float16 *dst = p.C + (int64_t)i * p.ldc + j;
-                if (VEC && j + 8 <= p.N) {
-                    *reinterpret_cast<h8 *>(dst) = o;
+                if (j + 8 <= p.N) {
+                    *reinterpret_cast<h8u *>(dst) = o;
                 } else {
 #pragma unroll
                     for (int e = 0; e < 8; ++e)

@@ -102,7 +102,7 @@ hipError_t launch_generic(const GemmArgs &a, hipStream_t s)
 {
     constexpr TileCfg c = GENERIC_TILE;
     dim3 grid((unsigned)(a.tiles_m * a.tiles_n)), block(64 * c.wm * c.wn);
-    hipLaunchKernelGGL((gemm_bias_act_generic<c.bm, c.bn, c.wm, c.wn, LA, LB, ACC16, false, PRO, DUAL>),
+    hipLaunchKernelGGL((gemm_bias_act_generic<c.bm, c.bn, c.wm, c.wn, LA, LB, ACC16, PRO, DUAL>),
                        grid, block, 0, s, a);
     return hipGetLastError();
 }
