@@ -106,11 +106,61 @@ def cpu_baseline(w, A, B, bias, P=None, Q=None, target_s=12.0):
                       f"fp64, {dt:.1f} s"}
 
 
+def time_graph(fns, launches, replays, torch):
+    """Average ms per launch of `launches` calls (cycling through fns)
+    captured in one HIP graph and replayed: device time without the host's
+    per-call launch cost."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for f in fns[:3]:
+            f()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(launches):
+            fns[i % len(fns)]()
+    g.replay()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(replays):
+        g.replay()
+    stop.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(stop) / (replays * launches)
+
+
+COLD_POOL_BYTES = 1 << 30
+
+
+def cold_operands(torch, dA, dB, M, N, nsets):
+    """nsets copies of (A, B, C) in distinct memory, same layouts and values,
+    so that rotating through them misses the caches (L2 and the 256 MB
+    last-level cache) on every launch."""
+    def pool(t):
+        if t.stride(-1) == 1:
+            p = torch.empty((nsets,) + tuple(t.shape), dtype=t.dtype, device=t.device)
+            p.copy_(t.unsqueeze(0).expand_as(p))
+            return [p[i] for i in range(nsets)]
+        tt = t.t()
+        p = torch.empty((nsets,) + tuple(tt.shape), dtype=t.dtype, device=t.device)
+        p.copy_(tt.unsqueeze(0).expand_as(p))
+        return [p[i].t() for i in range(nsets)]
+    outs = torch.empty((nsets, M, N), dtype=torch.float16, device=dA.device)
+    return list(zip(pool(dA), pool(dB), [outs[i] for i in range(nsets)]))
+
+
 def configs(args, np, torch, D, gba):
     """Every single-product workload configuration: layouts x accumulations,
-    the library's tile choice, fused launches timed like the headline.  The
-    roofline bound is HBM below the ridge point (peak flops / peak bytes)
-    and MFMA above it."""
+    the library's tile choice.  `us` is device time per launch from a
+    captured graph of back-to-back launches on the same (cache-resident)
+    operands; `us_eager` the same launches issued one by one from Python.
+    The roofline bound is HBM below the ridge point (peak flops / peak
+    bytes) and MFMA above it; HBM-bound rows also give a cold-cache figure
+    (`cold`), rotating through at least 1 GiB of operand copies."""
     ridge = PEAK_F16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
     for w in D.WORKLOADS.values():
         if w.extra:
@@ -118,6 +168,9 @@ def configs(args, np, torch, D, gba):
         A, B, bias = D.logical_inputs(w)
         dbias = torch.from_numpy(bias).cuda()
         out = torch.empty((w.M, w.N), dtype=torch.float16, device="cuda")
+        flops = 2.0 * w.M * w.N * w.K
+        nbytes = 2.0 * (w.M * w.K + w.K * w.N + w.M * w.N + w.N)
+        hbm = flops / nbytes < ridge
         for layout in w.layouts:
             la, lb = D.LAYOUT_NAMES[layout]
             dA = (torch.from_numpy(A).cuda() if la == D.ROW
@@ -125,20 +178,27 @@ def configs(args, np, torch, D, gba):
             dB = (torch.from_numpy(B).cuda() if lb == D.ROW
                   else torch.from_numpy(np.ascontiguousarray(B.T)).cuda().t())
             for acc in w.accum:
-                fn = lambda: gba.gemm_bias_act(dA, dB, dbias, act="relu", accum=acc, out=out)
-                ms = time_launches(fn, args.steps, args.warmup, torch)
-                flops = 2.0 * w.M * w.N * w.K
-                nbytes = 2.0 * (w.M * w.K + w.K * w.N + w.M * w.N + w.N)
+                call = lambda a, b, c: (lambda: gba.gemm_bias_act(a, b, dbias, act="relu", accum=acc, out=c))
+                ms_eager = time_launches(call(dA, dB, out), args.steps, args.warmup, torch)
+                ms = time_graph([call(dA, dB, out)], args.steps, 10, torch)
                 tf = flops / (ms * 1e-3) / 1e12
                 gbs = nbytes / (ms * 1e-3) / 1e9
-                hbm = flops / nbytes < ridge
-                print(json.dumps({
+                line = {
                     "workload": w.name, "M": w.M, "N": w.N, "K": w.K, "layout": layout, "accum": acc,
                     "tile": gba.select_tile(w.M, w.N, w.K, la, lb, acc), "us": round(ms * 1e3, 2),
-                    "TFLOP/s": round(tf, 1), "GB/s": round(gbs, 1),
+                    "us_eager": round(ms_eager * 1e3, 2), "TFLOP/s": round(tf, 1), "GB/s": round(gbs, 1),
                     "roofline": {"bound": "hbm" if hbm else "mfma",
                                  "frac": round(gbs / PEAK_HBM_GBS if hbm else tf / PEAK_F16_TFLOPS, 4)},
-                }), flush=True)
+                }
+                if hbm:
+                    nsets = -(-COLD_POOL_BYTES // int(nbytes))
+                    sets = cold_operands(torch, dA, dB, w.M, w.N, nsets)
+                    ms_cold = time_graph([call(*s) for s in sets], nsets, 3, torch)
+                    del sets
+                    gbs_cold = nbytes / (ms_cold * 1e-3) / 1e9
+                    line["cold"] = {"us": round(ms_cold * 1e3, 2), "GB/s": round(gbs_cold, 1),
+                                    "frac": round(gbs_cold / PEAK_HBM_GBS, 4), "sets": nsets}
+                print(json.dumps(line), flush=True)
 
 
 def main():
@@ -211,6 +271,20 @@ def main():
         idiom = "GEMM+bias+ReLU"
         chain = "GEMM, bias add, ReLU"
         plain_leg = "GEMM only (no bias, no activation)"
+
+        # context: the same problem through torch's library path (hipBLASLt
+        # GEMM, torch's elementwise kernels), the counterpart of the paper's
+        # library baseline
+        def lib_chain():
+            torch.matmul(dA, dB, out=out)
+            out.add_(dbias)
+            out.relu_()
+
+        def lib_addmm_relu():
+            torch.addmm(dbias, dA, dB, out=out)
+            out.relu_()
+        library = {"library_gemm": lambda: torch.matmul(dA, dB, out=out),
+                   "library_chain": lib_chain, "library_addmm_relu": lib_addmm_relu}
     elif P is None:
         # relu(A).B + bias -> ReLU; unfused: ReLU pass over A, then the fused GEMM
         a_relu = dA.clone()
@@ -222,6 +296,7 @@ def main():
             gba.relu_(a_relu)
             gba.gemm_bias_act(a_relu, dB, dbias, act="relu", out=out, tile=tile)
         idiom = "ReLU-prologue GEMM+bias+ReLU"
+        library = {}
         chain = "ReLU over A, GEMM+bias+ReLU"
         plain_leg = "GEMM+bias+ReLU without the prologue"
     else:
@@ -238,6 +313,7 @@ def main():
             gba.bias_add_(out, dbias)
             gba.relu_(out)
         idiom = "Add(GEMM,GEMM)+bias+ReLU"
+        library = {}
         chain = "GEMM, GEMM, add, bias add, ReLU"
         plain_leg = "GEMM+bias+ReLU of A.B alone"
 
@@ -247,12 +323,14 @@ def main():
     if args.fused_only:
         args.no_cpu = True
         ms_plain = ms_unfused = ms_fused2 = float("nan")
+        ms_library = {}
     else:
         # the comparison legs get the same warmup, then the fused kernel is
         # timed once more right after the unfused chain
         ms_plain = time_launches(plain, args.steps, args.warmup, torch)
         ms_unfused = time_launches(unfused, args.steps, args.warmup, torch)
         ms_fused2 = time_launches(fused, args.steps, 0, torch)
+        ms_library = {k: time_launches(f, args.steps, args.warmup, torch) for k, f in library.items()}
 
     flops = 2.0 * w.M * w.N * (w.K + K2)
     tflops = flops / (ms * 1e-3) / 1e12
@@ -299,6 +377,11 @@ def main():
             "unfused_chain_ms": round(ms_unfused, 5),
             "fused_vs_unfused_speedup": round(ms_unfused / ms, 3),
             "fused_algorithmic_GBps": round(algo_bytes / (ms * 1e-3) / 1e9, 1),
+            **({"library_legs": "torch: hipBLASLt GEMM (matmul / addmm with the bias), torch "
+                                "bias add and ReLU; context, same inputs",
+                **{f"{k}_ms": round(v, 5) for k, v in ms_library.items()},
+                "fused_vs_library_chain_speedup": round(ms_library["library_chain"] / ms, 3)}
+               if ms_library else {}),
         },
     }
     if args.report:

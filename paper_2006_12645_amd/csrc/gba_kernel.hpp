@@ -80,6 +80,25 @@ __device__ __forceinline__ int swz32(int r)
     return b0 | (b1 << 1) | (b2 << 2);
 }
 
+// Chunk permutations of the 16x16x32 path's LDS rows (conflict-free for
+// its fragment reads: 16 rows of one 16-row block at one chunk for A, the
+// permuted columns of perm16 for B).  swzA16 has period 16, so the A blocks
+// of a warp tile sit at fixed offsets from each other.
+__device__ __forceinline__ int swzA16(int r) { return ((r >> 1) & 3) | (((r ^ (r >> 3)) & 1) << 2); }
+__device__ __forceinline__ int swzB16(int r)
+{
+    return ((r >> 1) & 1) | (((r ^ (r >> 4)) & 1) << 1) | (((r ^ (r >> 3) ^ (r >> 5)) & 1) << 2);
+}
+
+// Chunk permutation SW: 0 swz32 (32x32x16 path), 1 swzA16, 2 swzB16.
+template <int SW>
+__device__ __forceinline__ int swz_sel(int r)
+{
+    if constexpr (SW == 1) return swzA16(r);
+    else if constexpr (SW == 2) return swzB16(r);
+    else return swz32(r);
+}
+
 // Column (inside a 32-column block of B) presented as MFMA row rho.  The
 // MFMA returns row rho = 8*(r/4) + 4*(lane/32) + r%4 in accumulator r of a
 // lane, which this maps to column 16*(lane/32) + r.
@@ -131,12 +150,15 @@ __device__ __forceinline__ void sched_slice()
 // row l / 8.  No registers hold the data and no LDS write instruction is
 // issued.  Instruction i of wave w fills rows 8*(NW*i + w) .. +7.  A chunk
 // at or beyond K is fetched with an out-of-range offset, for which the copy
-// writes zeros.
-template <int R, int NT>
+// writes zeros.  SW selects the chunk permutation (swz_sel).
+template <int R, int NT, int SW = 0>
 struct DmaCopy {
     static constexpr int NW = NT / 64;
     static constexpr int NI = R / (8 * NW);                   // instructions per wave per step
-    static constexpr int NV0 = (8 * NW) % 32 == 0 ? 1 : 32 / (8 * NW);
+    // rows of instructions NV apart differ by a multiple of the chunk
+    // permutation's period, so they share lane offsets
+    static constexpr int PER = SW == 2 ? 64 : 32;
+    static constexpr int NV0 = (8 * NW) % PER == 0 ? 1 : PER / (8 * NW);
     static constexpr int NV = NV0 < NI ? NV0 : NI;            // distinct lane offsets
     static constexpr int NLOAD = NI;
     static_assert(R % (8 * NW) == 0, "rows must divide evenly among the waves");
@@ -154,7 +176,7 @@ struct DmaCopy {
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
             const int row = 8 * (NW * v + w) + (l >> 3);
-            const int c = (l & 7) ^ swz32(row);
+            const int c = (l & 7) ^ swz_sel<SW>(row);
             voff[v] = (int)((l >> 3) * ldb2) + 16 * c;
             kq[v] = 8 * c;
         }

@@ -1,0 +1,403 @@
+// gba_kernel16.hpp -- the fast path on v_mfma_f32_16x16x32_f16 for operands
+// that are contiguous along the reduction (row-major A, column-major B).
+//
+// Same decomposition as gemm_bias_act_fast (block tile per workgroup, warp
+// tiles per wave, 64-deep reduction steps through direct global -> LDS
+// copies over NSTG stages, one barrier per step, epilogue in registers), with
+// the wave-level contraction on 16x16 output blocks, 32 deep per
+// instruction.  For the same work the 16x16x32 instruction reads and writes
+// a quarter of the accumulator registers that 32x32x16 does per instruction
+// (half per flop), and under the part's power limit this runs the MFMA pipes
+// at a markedly higher clock (measured on a GEMM-shaped loop with LDS
+// fragment reads: 1.70 against 1.44-1.52 PFLOP/s).
+//
+// Operand roles and store order.  As in the 32x32 path the MFMA "A" slot
+// takes columns of B and the "B" slot rows of A, so lane l holds, for every
+// 16x16 block, output row l % 16 and the four output columns presented as
+// MFMA rows 4*(l/16) .. 4*(l/16)+3.  The B columns are presented in the
+// order perm16: within each group of G blocks (16G columns), block t's MFMA
+// row rho is column 4G*(rho/4) + 4*(t%G) + rho%4, so across the group's G
+// blocks a lane holds 4G consecutive outputs of its row (16 for G = 4: two
+// 16-byte stores).
+//
+// Slices.  A 64-deep step is two 32-deep halves; each half is split into two
+// slices over the A blocks of the warp tile (TM/2 each), so a step has four
+// slices like the 32x32 path.  The A fragments of the next slice are read
+// during the current one; the B fragments of a half are read during the
+// slice before it (and used by both of its slices).
+#pragma once
+
+#include "gba_kernel.hpp"
+
+namespace gba {
+
+// Column (inside a warp tile's B columns) presented as MFMA row rho of
+// 16-column block t, with G blocks per group of consecutive outputs.
+template <int G>
+__device__ __forceinline__ int perm16(int t, int rho)
+{
+    return 16 * G * (t / G) + 4 * G * (rho >> 2) + 4 * (t % G) + (rho & 3);
+}
+
+template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool PRO, bool DUAL,
+          bool SPLIT>
+__global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmArgs p)
+{
+    constexpr int NTG = 64 * WM * WN;         // threads per k-group
+    constexpr int NT = NTG * SK;
+    constexpr int BK = 64;
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int TM = WTM / 16, TN = WTN / 16;   // 16x16 blocks of the warp tile
+    constexpr int TMH = TM / 2;                    // A blocks per slice
+    constexpr int G = TN < 4 ? TN : 4;             // B blocks per group of consecutive outputs
+    constexpr int ROWB = BK * 2;                   // bytes per LDS row
+    constexpr int SUB = (BM + BN) * ROWB;          // bytes per k-group sub-stage
+    constexpr int STAGE = SK * SUB;                // bytes per LDS stage
+    constexpr int NS = NSTG;
+    static_assert(LA == ROW && LB == COL, "16x16x32 path: reduction-contiguous operands");
+    static_assert((NS & (NS - 1)) == 0, "stage count must be a power of two");
+    static_assert(WTM % 32 == 0 && WTN % 32 == 0, "warp tile must be a multiple of 32x32");
+    static_assert(G >= 2 && TN % G == 0, "B blocks come in groups of two or four");
+    static_assert(!(ACC16 && SK > 1), "fp16 accumulation is defined for a single running sum");
+    static_assert(!SPLIT || (SK == 1 && !ACC16), "a split reduction needs one k-group and fp32 sums");
+    constexpr int PADN = BN + 4;               // fp32 row pitch of the split-K partial tiles
+    constexpr int RED = SK > 1 ? SK * BM * PADN * 4 : 0;
+    constexpr int LDS_BYTES = NS * STAGE > RED ? NS * STAGE : RED;
+
+    __shared__ __attribute__((aligned(16))) char lds[LDS_BYTES];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int grp = wave / (WM * WN);         // k-group
+    const int gtid = tid - grp * NTG;         // thread index inside the k-group
+    const int wm = (wave % (WM * WN)) % WM, wn = (wave % (WM * WN)) / WM;
+    const int l16 = lane & 15, g4 = lane >> 4;
+
+    int tile_id = blockIdx.x, kspl = 0;
+    if constexpr (SPLIT) {
+        tile_id = __builtin_amdgcn_readfirstlane((int)blockIdx.x / p.splits);
+        kspl = __builtin_amdgcn_readfirstlane((int)blockIdx.x - tile_id * p.splits);
+    }
+    int tm, tn;
+    tile_coords(tile_id, SPLIT ? p.tiles_m * p.tiles_n : (int)gridDim.x, p.tiles_m, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int mc = m0 + BM <= p.M ? m0 : p.M - BM;
+    const int nc = n0 + BN <= p.N ? n0 : p.N - BN;
+
+    using CopyA = DmaCopy<BM, NTG, 1>;
+    using CopyB = DmaCopy<BN, NTG, 2>;
+    CopyA ca;
+    CopyB cb;
+
+    // Fragment byte offsets inside a stage, per 32-deep half h: A block s is
+    // 16 rows (2048 bytes) after block 0 (swzA16 has period 16); each B
+    // block has its own rows.
+    int offa[2], offb[2][TN];
+    {
+        const int ra = wm * WTM + l16;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) offa[h] = ra * ROWB + (((4 * h + g4) ^ swzA16(l16)) * 16);
+#pragma unroll
+        for (int t = 0; t < TN; ++t) {
+            const int rb = wn * WTN + perm16<G>(t, l16);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) offb[h][t] = (BM + rb) * ROWB + (((4 * h + g4) ^ swzB16(rb)) * 16);
+        }
+    }
+
+    f4 acc[TN][TM];
+#pragma unroll
+    for (int t = 0; t < TN; ++t)
+#pragma unroll
+        for (int s = 0; s < TM; ++s) acc[t][s] = f4{0.f, 0.f, 0.f, 0.f};
+
+    // A fragments of two slices, B fragments of two halves.
+    h8 fa[2][TMH], fb[2][TN];
+    auto read_a = [&](int buf, const char *stage, int h, int q) {
+#pragma unroll
+        for (int s = 0; s < TMH; ++s)
+            fa[buf][s] = *reinterpret_cast<const h8 *>(stage + offa[h] + (q * TMH + s) * 16 * ROWB);
+    };
+    auto read_b = [&](int buf, const char *stage, int h) {
+#pragma unroll
+        for (int t = 0; t < TN; ++t) fb[buf][t] = *reinterpret_cast<const h8 *>(stage + offb[h][t]);
+    };
+    // The slice's MFMAs: A blocks q*TMH .. q*TMH+TMH-1 of half `bbuf`.
+    auto mfmas = [&](int abuf, int bbuf, int q) {
+        if constexpr (PRO) {
+#pragma unroll
+            for (int s = 0; s < TMH; ++s) fa[abuf][s] = relu_h8(fa[abuf][s]);
+        }
+#pragma unroll
+        for (int t = 0; t < TN; ++t)
+#pragma unroll
+            for (int s = 0; s < TMH; ++s)
+                acc[t][q * TMH + s] =
+                    __builtin_amdgcn_mfma_f32_16x16x32_f16(fb[bbuf][t], fa[abuf][s], acc[t][q * TMH + s], 0, 0, 0);
+    };
+    auto round16 = [&]() {
+        // fp16 accumulation: the running sum is rounded to fp16 at the end of
+        // every aligned 32-deep group of k (after both slices of a half)
+        if constexpr (ACC16) {
+#pragma unroll
+            for (int t = 0; t < TN; ++t)
+#pragma unroll
+                for (int s = 0; s < TM; ++s)
+#pragma unroll
+                    for (int e = 0; e < 4; e += 2) {
+                        const f2v r = round_f16x2(f2v{acc[t][s][e], acc[t][s][e + 1]});
+                        acc[t][s][e] = r[0];
+                        acc[t][s][e + 1] = r[1];
+                    }
+        }
+    };
+    auto negate_acc = [&]() {
+#pragma unroll
+        for (int t = 0; t < TN; ++t)
+#pragma unroll
+            for (int s = 0; s < TM; ++s) acc[t][s] = -acc[t][s];
+    };
+
+    constexpr int NM = TN * TMH;              // MFMAs per slice
+    constexpr int NRA = TMH, NRB = TMH + TN;  // fragment reads of slices 0, 2 and of slices 1, 3
+    constexpr int NL = CopyA::NLOAD + CopyB::NLOAD;
+    constexpr int VM_AT_BARRIER = (NS - 2) * NL;
+    char *const mine = lds + grp * SUB;
+
+    // The row bias of this lane's output columns (4G consecutive per group
+    // of G blocks), loaded before the reduction.
+    constexpr int NGRP = TN / G;
+    h8 brow[SK == 1 ? NGRP : 1][G / 2];
+    if constexpr (SK == 1) {
+        if (p.bias_kind == BIAS_ROW) {
+#pragma unroll
+            for (int tg = 0; tg < NGRP; ++tg) {
+                const _Float16 *bp = p.bias + nc + wn * WTN + 16 * G * tg + 4 * G * g4;
+#pragma unroll
+                for (int v = 0; v < G / 2; ++v) brow[tg][v] = *reinterpret_cast<const h8 *>(bp + 8 * v);
+            }
+        }
+    }
+
+#pragma unroll 1
+    for (int seg = 0; seg < (DUAL ? 2 : 1); ++seg) {
+        const _Float16 *const X = seg == 0 ? p.A : p.P;
+        const _Float16 *const Y = seg == 0 ? p.B : p.Q;
+        const int64_t ldx = seg == 0 ? p.lda : p.ldp;
+        const int64_t ldy = seg == 0 ? p.ldb : p.ldq;
+        const int Kseg = seg == 0 ? p.K : p.K2;
+        if (seg == 1) {
+            __syncthreads();
+            if (p.sub) negate_acc();
+        }
+        ca.init(ldx, gtid);
+        cb.init(ldy, gtid);
+
+        auto rsrc_a = [&](int k0) { return make_rsrc(X + (int64_t)mc * ldx + k0, MAX_RECORDS); };
+        auto rsrc_b = [&](int k0) { return make_rsrc(Y + (int64_t)nc * ldy + k0, MAX_RECORDS); };
+        const int nk_seg = (Kseg + SK * BK - 1) / (SK * BK);
+        int s_lo = 0, s_hi = nk_seg;
+        if constexpr (SPLIT) {
+            const int off = seg == 0 ? 0 : (p.K + SK * BK - 1) / (SK * BK);
+            const int lo = kspl * p.split_steps - off, hi = lo + p.split_steps;
+            s_lo = __builtin_amdgcn_readfirstlane(lo < 0 ? 0 : (lo > nk_seg ? nk_seg : lo));
+            s_hi = __builtin_amdgcn_readfirstlane(hi < 0 ? 0 : (hi > nk_seg ? nk_seg : hi));
+        }
+        const int nk = s_hi - s_lo;
+
+        auto copy_step = [&](int s, char *stage) {
+            const int k0 = __builtin_amdgcn_readfirstlane((((s < nk ? s : nk - 1) + s_lo) * SK + grp) * BK);
+            const int kleft = s < nk ? Kseg - k0 : 0;
+            const auto ra = rsrc_a(k0);
+            const auto rb = rsrc_b(k0);
+            ca.dma(ra, stage, kleft);
+            cb.dma(rb, stage + BM * ROWB, kleft);
+        };
+
+        if (nk > 0) {
+#pragma unroll
+            for (int s = 0; s < NS; ++s) copy_step(s, mine + s * STAGE);
+            __builtin_amdgcn_sched_barrier(0);
+            wait_vm_lgkm0<(NS - 1) * NL>();
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+            read_a(0, mine, 0, 0);
+            read_b(0, mine, 0);
+        }
+
+        // One reduction step.  On entry LDS stage `cur` holds step kt, steps
+        // kt+1 .. kt+NS-1 are under way into the other stages, fa[0] holds
+        // the A fragments of slice 0 and fb[0] the B fragments of half 0.
+        for (int kt = 0; kt < nk; ++kt) {
+            char *cur = mine + (kt & (NS - 1)) * STAGE;
+            char *nxt = mine + ((kt + 1) & (NS - 1)) * STAGE;
+            // slice 0: half 0, first A blocks
+            read_a(1, cur, 0, 1);
+            mfmas(0, 0, 0);
+            sched_slice<NM, NRA, 0, 0, false>();
+            // slice 1: half 0, second A blocks (B fragments of half 1 in flight)
+            read_a(0, cur, 1, 0);
+            read_b(1, cur, 1);
+            mfmas(1, 0, 1);
+            round16();
+            sched_slice<NM, NRB, 0, 0, false>();
+            // slice 2: half 1, first A blocks
+            read_a(1, cur, 1, 1);
+            mfmas(0, 1, 0);
+            sched_slice<NM, NRA, 0, 0, false>();
+            // Step kt+1 complete in LDS for every wave; every read of `cur` done.
+            if constexpr (VM_AT_BARRIER == 0) {
+                __builtin_amdgcn_s_waitcnt(0);
+                __syncthreads();
+            } else {
+                __builtin_amdgcn_sched_barrier(0);
+                wait_vm_lgkm0<VM_AT_BARRIER>();
+                __builtin_amdgcn_s_barrier();
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            // slice 3: half 1, second A blocks, plus the first fragments of
+            // step kt+1 and the copies of step kt+NS (into `cur`, now free)
+            read_a(0, nxt, 0, 0);
+            read_b(0, nxt, 0);
+            mfmas(1, 1, 1);
+            round16();
+            copy_step(kt + NS, cur);
+            sched_slice<NM, NRB, 0x020, NL, false>();
+        }
+
+        __builtin_amdgcn_s_waitcnt(0);
+        if (seg == 1 && p.sub) negate_acc();
+    }
+
+    if constexpr (SPLIT) {
+        {
+            // Partial tile of this split to the workspace, each thread's 4
+            // accumulators of a 16x16 block as one 16-byte write.
+            float *const part = p.ws + (size_t)tile_id * p.splits * (BM * BN);
+#pragma unroll
+            for (int t = 0; t < TN; ++t)
+#pragma unroll
+                for (int s = 0; s < TM; ++s)
+                    *reinterpret_cast<f4 *>(part + (size_t)kspl * (BM * BN) + ((t * TM + s) * NT + tid) * 4) =
+                        acc[t][s];
+            __syncthreads();
+            __shared__ int last_split;
+            if (tid == 0) {
+                const unsigned before = __hip_atomic_fetch_add(p.counters + tile_id, 1u, __ATOMIC_RELEASE,
+                                                               __HIP_MEMORY_SCOPE_AGENT);
+                last_split = before == (unsigned)(p.splits - 1);
+                if (last_split) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            }
+            __syncthreads();
+            if (!__builtin_amdgcn_readfirstlane(last_split)) return;
+#pragma unroll
+            for (int t = 0; t < TN; ++t)
+#pragma unroll
+                for (int s = 0; s < TM; ++s) acc[t][s] = f4{0.f, 0.f, 0.f, 0.f};
+            for (int j = 0; j < p.splits; ++j) {
+#pragma unroll
+                for (int t = 0; t < TN; ++t)
+#pragma unroll
+                    for (int s = 0; s < TM; ++s)
+                        acc[t][s] += *reinterpret_cast<const f4 *>(part + (size_t)j * (BM * BN) +
+                                                                   ((t * TM + s) * NT + tid) * 4);
+            }
+            if (tid == 0)
+                __hip_atomic_store(p.counters + tile_id, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+
+    if constexpr (SK > 1) {
+        // Split-K: every k-group writes its partial tile to LDS (fp32, rows
+        // padded by 4 floats), then all threads sum the SK partials in group
+        // order, apply the epilogue and store 8 contiguous outputs each.
+        __syncthreads();
+        float *part = reinterpret_cast<float *>(lds);
+#pragma unroll
+        for (int t = 0; t < TN; ++t)
+#pragma unroll
+            for (int s = 0; s < TM; ++s) {
+                const int i = wm * WTM + 16 * s + l16;
+                const int j = wn * WTN + 16 * G * (t / G) + 4 * G * g4 + 4 * (t % G);
+                *reinterpret_cast<f4 *>(part + (grp * BM + i) * PADN + j) = acc[t][s];
+            }
+        __syncthreads();
+        constexpr int CPR = BN / 8;
+        for (int c = tid; c < BM * CPR; c += NT) {
+            const int i = c / CPR, j = (c % CPR) * 8;
+            float x[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[e] = 0.f;
+#pragma unroll
+            for (int g = 0; g < SK; ++g) {
+                const f4 *src = reinterpret_cast<const f4 *>(part + (g * BM + i) * PADN + j);
+                const f4 a0 = src[0], a1 = src[1];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    x[e] += a0[e];
+                    x[4 + e] += a1[e];
+                }
+            }
+            if (p.bias_kind != BIAS_NONE) {
+                const _Float16 *bp = p.bias_kind == BIAS_ROW ? p.bias + nc + j
+                                                             : p.bias + (int64_t)(mc + i) * p.ldbias + nc + j;
+                const h8 bv = *reinterpret_cast<const h8 *>(bp);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[e] += p.bias_sign * (float)bv[e];
+            }
+            activate(p.act, x);
+            h8 o;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o[e] = (_Float16)x[e];
+            if (mc + i >= m0 && nc + j >= n0)
+                *reinterpret_cast<h8 *>(p.C + (int64_t)(mc + i) * p.ldc + nc + j) = o;
+        }
+        return;
+    }
+
+    // Epilogue on registers: per A block and group of G B blocks a lane
+    // holds 4G consecutive outputs of one row: +/- bias, activation, fp16,
+    // 16-byte stores (each guarded so an output shared with a neighbouring
+    // tile is stored by its owner only).  Row blocks outermost.
+#pragma unroll
+    for (int s = 0; s < TM; ++s) {
+#pragma unroll
+        for (int tg = 0; tg < NGRP; ++tg) {
+            const int i = mc + wm * WTM + 16 * s + l16;
+            const int j = nc + wn * WTN + 16 * G * tg + 4 * G * g4;
+            float x[4 * G];
+#pragma unroll
+            for (int u = 0; u < G; ++u)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) x[4 * u + r] = acc[tg * G + u][s][r];
+            if (p.bias_kind == BIAS_ROW) {
+#pragma unroll
+                for (int v = 0; v < G / 2; ++v)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) x[8 * v + e] += p.bias_sign * (float)brow[tg][v][e];
+            } else if (p.bias_kind == BIAS_FULL) {
+                const _Float16 *bp = p.bias + (int64_t)i * p.ldbias + j;
+#pragma unroll
+                for (int v = 0; v < G / 2; ++v) {
+                    const h8 bv = *reinterpret_cast<const h8 *>(bp + 8 * v);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) x[8 * v + e] += p.bias_sign * (float)bv[e];
+                }
+            }
+            activate(p.act, x);
+            if (i >= m0) {
+                _Float16 *dst = p.C + (int64_t)i * p.ldc + j;
+#pragma unroll
+                for (int v = 0; v < G / 2; ++v) {
+                    h8 o;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) o[e] = (_Float16)x[8 * v + e];
+                    if (j + 8 * v >= n0) *reinterpret_cast<h8 *>(dst + 8 * v) = o;
+                }
+            }
+        }
+    }
+}
+
+}  // namespace gba

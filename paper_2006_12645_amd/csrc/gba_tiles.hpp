@@ -12,6 +12,7 @@
 #include <hip/hip_runtime.h>
 
 #include "gba_kernel.hpp"
+#include "gba_kernel16.hpp"
 #include "gba_kernel_generic.hpp"
 
 namespace gba {
@@ -75,8 +76,13 @@ hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
 {
     // one workgroup per output tile, times the splits of its reduction
     dim3 grid((unsigned)(a.tiles_m * a.tiles_n * (SPLIT ? a.splits : 1))), block(64 * WM * WN * SK);
-    hipLaunchKernelGGL((gemm_bias_act_fast<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, PRO, DUAL, SPLIT>), grid,
-                       block, 0, s, a);
+    // reduction-contiguous operands on 16x16x32 MFMAs, the others on 32x32x16
+    if constexpr (LA == ROW && LB == COL)
+        hipLaunchKernelGGL((gemm_bias_act_fast16<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, PRO, DUAL, SPLIT>), grid,
+                           block, 0, s, a);
+    else
+        hipLaunchKernelGGL((gemm_bias_act_fast<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, PRO, DUAL, SPLIT>), grid,
+                           block, 0, s, a);
     return hipGetLastError();
 }
 
