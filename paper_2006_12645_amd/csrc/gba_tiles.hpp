@@ -76,8 +76,10 @@ hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
 {
     // one workgroup per output tile, times the splits of its reduction
     dim3 grid((unsigned)(a.tiles_m * a.tiles_n * (SPLIT ? a.splits : 1))), block(64 * WM * WN * SK);
-    // reduction-contiguous operands on 16x16x32 MFMAs, the others on 32x32x16
-    if constexpr (LA == ROW && LB == COL)
+    // reduction-contiguous operands on 16x16x32 MFMAs, the others on
+    // 32x32x16; so is the 4-wave 256x256 tile, whose 64 16x16 accumulator
+    // blocks per wave do not fit the registers without spilling
+    if constexpr (LA == ROW && LB == COL && !(BM * BN == 256 * 256 && WM * WN == 4))
         hipLaunchKernelGGL((gemm_bias_act_fast16<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, PRO, DUAL, SPLIT>), grid,
                            block, 0, s, a);
     else
