@@ -86,30 +86,14 @@ int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum);
 //     that makes at most 256 -- then 32x32.
 // The 256x128 and 128x256 tiles were never the fastest in those sweeps and
 // are only used when asked for.
-//
-// With reduction-contiguous operands (row-major A, column-major B: the
-// kernels on 16x16x32 MFMAs) and fp32 accumulation, three changes, fitted
-// to sweeps of those kernels (one set of shapes, checked on two others):
-//   * 128x128 with two k-groups for 128 to 256 workgroups over a reduction
-//     of 1024 or more (after the 256x256 cases);
-//   * 64x64 with two k-groups for 160 to 256 workgroups from K = 512 where
-//     the rest of the rule would take 64x64, 32x64 or a k-group 32-row tile;
-//   * 32x64 instead of 64x64 below 320 workgroups of 64x64 from K = 1536.
-int select_tile(int64_t M, int64_t N, int64_t K, int accum, bool rc)
+int select_tile(int64_t M, int64_t N, int64_t K, int accum)
 {
     auto tiles = [&](int t) -> int64_t {
         return tile_fits(t, M, N) ? ceil_div(M, TILES[t].bm) * ceil_div(N, TILES[t].bn) : 0;
     };
-    const bool fast16 = rc && accum == GBA_ACC_F32;
     if (tiles(1) >= 136) return 1;
     if (tiles(1) >= 112 && tiles(4) > 512) return 1;  // 128x128 would need a second round
-    if (fast16 && K >= 1024 && tiles(14) >= 128 && tiles(14) <= 256) return 14;
-    const int t = select_tile_rest(M, N, K, accum);
-    if (fast16) {
-        if ((t == 6 || t == 8 || t == 12 || t == 13) && K >= 512 && tiles(11) >= 160 && tiles(11) <= 256) return 11;
-        if (t == 6 && K >= 1536 && tiles(6) < 320 && tile_fits(8, M, N)) return 8;
-    }
-    return t;
+    return select_tile_rest(M, N, K, accum);
 }
 
 // The rule below the 256x256 cases.
@@ -224,8 +208,7 @@ Plan make_plan(const gba_fused_desc &d, bool may_split)
     const bool fp32 = d.accum == GBA_ACC_F32;
     int64_t auto_s = 1;
     if (may_split && d.split_k == 0 && !tile_ok && fp32) auto_s = auto_splits(d.M, d.N, ktot);
-    pl.tile = tile_ok ? d.tile_id : (auto_s > 1 ? AUTO_SPLIT_TILE : select_tile(d.M, d.N, ktot, d.accum,
-                                                                                  d.layoutA == GBA_ROW_MAJOR && d.layoutB == GBA_COL_MAJOR));
+    pl.tile = tile_ok ? d.tile_id : (auto_s > 1 ? AUTO_SPLIT_TILE : select_tile(d.M, d.N, ktot, d.accum));
     if (pl.tile >= 0 && !fast_path_ok(d)) pl.tile = -1;
     pl.cfg = pl.tile >= 0 ? TILES[pl.tile] : GENERIC_TILE;
     pl.tiles_m = ceil_div(d.M, pl.cfg.bm);
@@ -497,7 +480,7 @@ extern "C" int gba_select_tile(gba_layout layoutA, gba_layout layoutB, int64_t M
     if (!is_layout(layoutA) || !is_layout(layoutB)) return -1;
     if (accum != GBA_ACC_F32 && accum != GBA_ACC_F16) return -1;
     if (M < 0 || N < 0 || K < 0 || M > INT_MAX || N > INT_MAX || K > INT_MAX) return -1;
-    return select_tile(M, N, K, accum, layoutA == GBA_ROW_MAJOR && layoutB == GBA_COL_MAJOR);  // -1 also when the general path would run
+    return select_tile(M, N, K, accum);  // -1 also when the general path would run
 }
 
 extern "C" gba_status gba_bias_add_f16(int64_t M, int64_t N, void *C, int64_t ldc, const void *bias,

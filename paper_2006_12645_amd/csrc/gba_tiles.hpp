@@ -70,16 +70,24 @@ struct LayoutTable {
     LaunchFn generic[2];
 };
 
+// Which tiles run the 16x16x32 kernel (gemm_bias_act_fast16).
+constexpr bool use_fast16(int la, int lb, int bm, int bn, int wm, int wn)
+{
+    return la == ROW && lb == COL && bm == 256 && bn == 256 && wm * wn == 8;
+}
+
 template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool PRO, bool DUAL,
           bool SPLIT = false>
 hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
 {
     // one workgroup per output tile, times the splits of its reduction
     dim3 grid((unsigned)(a.tiles_m * a.tiles_n * (SPLIT ? a.splits : 1))), block(64 * WM * WN * SK);
-    // reduction-contiguous operands on 16x16x32 MFMAs, the others on
-    // 32x32x16; so is the 4-wave 256x256 tile, whose 64 16x16 accumulator
-    // blocks per wave do not fit the registers without spilling
-    if constexpr (LA == ROW && LB == COL && !(BM * BN == 256 * 256 && WM * WN == 4))
+    // The 8-wave 256x256 tile with reduction-contiguous operands runs on
+    // 16x16x32 MFMAs, everything else on 32x32x16 (measured per tile: the
+    // 16x16x32 kernels of the other tiles were up to 20% slower, the 4-wave
+    // 256x256 one does not fit its 64 accumulator blocks per wave in
+    // registers)
+    if constexpr (use_fast16(LA, LB, BM, BN, WM, WN))
         hipLaunchKernelGGL((gemm_bias_act_fast16<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, PRO, DUAL, SPLIT>), grid,
                            block, 0, s, a);
     else
