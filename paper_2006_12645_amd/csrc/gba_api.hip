@@ -84,15 +84,22 @@ int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum);
 //     accumulation and K >= 768, by 32x32 with four k-groups when that
 //     makes at most 128 workgroups, else by 32x64 with four k-groups when
 //     that makes at most 256 -- then 32x32.
-// The 256x128 and 128x256 tiles were never the fastest in those sweeps and
-// are only used when asked for.
-int select_tile(int64_t M, int64_t N, int64_t K, int accum)
+// The 4-wave 256x128 and 128x256 tiles were never the fastest in those
+// sweeps and are only used when asked for.  With reduction-contiguous
+// operands and fp32 accumulation (the 16x16x32 kernels), the 8-wave
+// 256x128 / 128x256 tiles (long side along the longer output side) take
+// the shapes where they make one round of 224 to 256 workgroups (fitted
+// the same way, on one sweep and checked on another: 8192x1024x4096 65.4
+// against 69.2 us on 128x128).
+int select_tile(int64_t M, int64_t N, int64_t K, int accum, bool rc)
 {
     auto tiles = [&](int t) -> int64_t {
         return tile_fits(t, M, N) ? ceil_div(M, TILES[t].bm) * ceil_div(N, TILES[t].bn) : 0;
     };
     if (tiles(1) >= 136) return 1;
     if (tiles(1) >= 112 && tiles(4) > 512) return 1;  // 128x128 would need a second round
+    const int t8w = N > M ? 17 : 16;
+    if (rc && accum == GBA_ACC_F32 && tiles(t8w) >= 224 && tiles(t8w) <= 256) return t8w;
     return select_tile_rest(M, N, K, accum);
 }
 
@@ -208,7 +215,8 @@ Plan make_plan(const gba_fused_desc &d, bool may_split)
     const bool fp32 = d.accum == GBA_ACC_F32;
     int64_t auto_s = 1;
     if (may_split && d.split_k == 0 && !tile_ok && fp32) auto_s = auto_splits(d.M, d.N, ktot);
-    pl.tile = tile_ok ? d.tile_id : (auto_s > 1 ? AUTO_SPLIT_TILE : select_tile(d.M, d.N, ktot, d.accum));
+    pl.tile = tile_ok ? d.tile_id : (auto_s > 1 ? AUTO_SPLIT_TILE : select_tile(d.M, d.N, ktot, d.accum,
+                                                                                  d.layoutA == GBA_ROW_MAJOR && d.layoutB == GBA_COL_MAJOR));
     if (pl.tile >= 0 && !fast_path_ok(d)) pl.tile = -1;
     pl.cfg = pl.tile >= 0 ? TILES[pl.tile] : GENERIC_TILE;
     pl.tiles_m = ceil_div(d.M, pl.cfg.bm);
@@ -480,7 +488,7 @@ extern "C" int gba_select_tile(gba_layout layoutA, gba_layout layoutB, int64_t M
     if (!is_layout(layoutA) || !is_layout(layoutB)) return -1;
     if (accum != GBA_ACC_F32 && accum != GBA_ACC_F16) return -1;
     if (M < 0 || N < 0 || K < 0 || M > INT_MAX || N > INT_MAX || K > INT_MAX) return -1;
-    return select_tile(M, N, K, accum);  // -1 also when the general path would run
+    return select_tile(M, N, K, accum, layoutA == GBA_ROW_MAJOR && layoutB == GBA_COL_MAJOR);  // -1 also when the general path would run
 }
 
 extern "C" gba_status gba_bias_add_f16(int64_t M, int64_t N, void *C, int64_t ldc, const void *bias,

@@ -19,7 +19,7 @@ torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
 LAYOUTS = ["RR", "RC", "CR", "CC"]
-NUM_TILES = 16
+NUM_TILES = 18
 ACT = {"none": O.ACT_NONE, "relu": O.ACT_RELU, "sigmoid": O.ACT_SIGMOID, "tanh": O.ACT_TANH}
 
 
@@ -224,6 +224,30 @@ def test_integer_exact(layout, accum, second):
     for kw in (dict(prologue=True, second=second, bias_op="sub", act="none"),
                dict(prologue=False, second=second, bias_op="add", act="relu")):
         got = pr.gpu(layout, accum=accum, **kw).astype(np.float64)
+        ref = pr.oracle(**kw)
+        assert np.array_equal(got, ref), (kw, np.abs(got - ref).max())
+
+
+# The 256x256 eight-wave tile runs on 16x16x32 MFMAs for reduction-contiguous
+# operands: its own checks, on sizes that shift its edge tiles inside the matrix.
+
+@pytest.mark.parametrize("act", ["sigmoid", "tanh"])
+def test_headline_tile_activations(act):
+    announce("tile 1 activation", act)
+    pr = Problem(731, 600, 536, 328, dist="mlp")
+    got = pr.gpu("RC", act=act, bias_op="sub", tile=1)
+    ref = pr.oracle(act=act, bias_op="sub")
+    U.assert_close(got, ref, what=f"tile 1 {act}")
+    assert np.abs(got.astype(np.float64) - ref).max() <= 2e-3
+
+
+@pytest.mark.parametrize("accum", ["f32", "f16"])
+def test_headline_tile_integer_exact(accum):
+    announce("tile 1 integer", accum)
+    pr = Problem(781, 600, 536, 392, K2=136, dist="int", full_bias=True)
+    for kw in (dict(prologue=True, second="sub", bias_op="sub", act="none"),
+               dict(prologue=False, second="add", bias_op="add", act="relu")):
+        got = pr.gpu("RC", accum=accum, tile=1, **kw).astype(np.float64)
         ref = pr.oracle(**kw)
         assert np.array_equal(got, ref), (kw, np.abs(got - ref).max())
 
