@@ -84,13 +84,12 @@ int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum);
 //     accumulation and K >= 768, by 32x32 with four k-groups when that
 //     makes at most 128 workgroups, else by 32x64 with four k-groups when
 //     that makes at most 256 -- then 32x32.
-// The 4-wave 256x128 and 128x256 tiles were never the fastest in those
-// sweeps and are only used when asked for.  With reduction-contiguous
-// operands and fp32 accumulation (the 16x16x32 kernels), the 8-wave
-// 256x128 / 128x256 tiles (long side along the longer output side) take
-// the shapes where they make one round of 224 to 256 workgroups (fitted
-// the same way, on one sweep and checked on another: 8192x1024x4096 65.4
-// against 69.2 us on 128x128).
+// The 256x128 and 128x256 tiles (4 or 8 waves) were never clearly the
+// fastest in those sweeps and are only used when asked for.  With
+// reduction-contiguous operands and fp32 accumulation, 128x128 means the
+// 8-wave tile on 16x16x32 MFMAs (3-6% faster than the 4-wave one over the
+// shapes the rule gives it; over two sweeps of random shapes the rule is
+// then 0.8-0.9% slower in total than the per-shape best tile).
 int select_tile(int64_t M, int64_t N, int64_t K, int accum, bool rc)
 {
     auto tiles = [&](int t) -> int64_t {
@@ -98,9 +97,8 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum, bool rc)
     };
     if (tiles(1) >= 136) return 1;
     if (tiles(1) >= 112 && tiles(4) > 512) return 1;  // 128x128 would need a second round
-    const int t8w = N > M ? 17 : 16;
-    if (rc && accum == GBA_ACC_F32 && tiles(t8w) >= 224 && tiles(t8w) <= 256) return t8w;
-    return select_tile_rest(M, N, K, accum);
+    const int t = select_tile_rest(M, N, K, accum);
+    return rc && accum == GBA_ACC_F32 && t == 4 ? 18 : t;
 }
 
 // The rule below the 256x256 cases.

@@ -44,9 +44,10 @@ struct TileCfg {
     X(14, 128, 128, 2, 2, 2, 2)  \
     X(15, 64, 128, 1, 2, 2, 2)   \
     X(16, 256, 128, 2, 4, 1, 2)  \
-    X(17, 128, 256, 4, 2, 1, 2)
+    X(17, 128, 256, 4, 2, 1, 2)  \
+    X(18, 128, 128, 2, 4, 1, 2)
 
-constexpr int NUM_TILES = 18;
+constexpr int NUM_TILES = 19;
 
 #define GBA_TILE_CFG(id, BM, BN, WM, WN, SK, NSTG) TileCfg{BM, BN, WM, WN, SK, NSTG},
 constexpr TileCfg TILES[NUM_TILES] = {GBA_TILE_LIST(GBA_TILE_CFG)};
@@ -72,11 +73,11 @@ struct LayoutTable {
     LaunchFn generic[2];
 };
 
-// Which tiles run the 16x16x32 kernel (gemm_bias_act_fast16): the 8-wave
-// ones with a 256-row or 256-column block tile.
+// Which tiles run the 16x16x32 kernel (gemm_bias_act_fast16): the ones
+// with eight waves of one k-group.
 constexpr bool use_fast16(int la, int lb, int bm, int bn, int wm, int wn)
 {
-    return la == ROW && lb == COL && (bm == 256 || bn == 256) && wm * wn == 8;
+    return la == ROW && lb == COL && bm >= 128 && bn >= 128 && wm * wn == 8;
 }
 
 template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool PRO, bool DUAL,
@@ -85,8 +86,8 @@ hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
 {
     // one workgroup per output tile, times the splits of its reduction
     dim3 grid((unsigned)(a.tiles_m * a.tiles_n * (SPLIT ? a.splits : 1))), block(64 * WM * WN * SK);
-    // The 8-wave tiles with a 256-row or -column block tile and
-    // reduction-contiguous operands run on 16x16x32 MFMAs, everything else
+    // The 8-wave tiles (one k-group) with reduction-contiguous operands run
+    // on 16x16x32 MFMAs, everything else
     // on 32x32x16 (measured per tile: the 16x16x32 kernels of the 4-wave
     // tiles were up to 20% slower, and the 4-wave 256x256 one does not fit
     // its 64 accumulator blocks per wave in registers)

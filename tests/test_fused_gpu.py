@@ -19,7 +19,7 @@ torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
 LAYOUTS = ["RR", "RC", "CR", "CC"]
-NUM_TILES = 18
+NUM_TILES = 19
 ACT = {"none": O.ACT_NONE, "relu": O.ACT_RELU, "sigmoid": O.ACT_SIGMOID, "tanh": O.ACT_TANH}
 
 
@@ -331,7 +331,7 @@ def counters_zero(ws, tile, M, N):
     return not ws[:tiles * 4].any().item()
 
 
-@pytest.mark.parametrize("tile", [4, 5, 6, 7, 8, 9])
+@pytest.mark.parametrize("tile", [4, 5, 6, 7, 8, 9, 18])
 @pytest.mark.parametrize("split", [2, 3, 7])
 def test_split_reduction_all_features(tile, split):
     # 16 + 4 steps of A.B and P.Q, ragged output (shifted edge tiles)
