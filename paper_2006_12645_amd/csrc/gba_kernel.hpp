@@ -215,7 +215,13 @@ __device__ __forceinline__ int bswT(int j)
 // rows RPI * g .. RPI * g + RPI - 1, lane l the 16-byte chunk at byte 16 l,
 // fetched from the global chunk that the block swizzle puts there.  Rows at
 // or beyond K are fetched with an out-of-range offset and become zeros.
-template <int R, int NT>
+// 16-element group permutation of reduction row k of an M- or N-contiguous
+// tile on the 16x16x32 path: its fragment reads touch, per half-wave, 16
+// consecutive elements of eight rows k0 + {0..3, 8..11}, which this spreads
+// over eight distinct 32-byte bank groups.
+__device__ __forceinline__ int fT16(int k) { return (k & 3) | (((k >> 3) & 1) << 2); }
+
+template <int R, int NT, int SW = 0>
 struct DmaCopyT {
     static constexpr int NW = NT / 64;
     static constexpr int CPR = R / 8;             // 16-byte chunks per row
@@ -223,6 +229,7 @@ struct DmaCopyT {
     static constexpr int NI = 64 / (RPI * NW);    // instructions per wave per step
     static constexpr int NLOAD = NI;
     static_assert(R >= 32 && R <= 512 && (R & (R - 1)) == 0, "rows of 32 to 512 elements");
+    static_assert(SW == 0 || R >= 128, "the 16x16x32 permutation needs 8 or more groups per row");
     static_assert(64 % (RPI * NW) == 0, "rows must divide evenly among the waves");
 
     int voff[NI];  // lane byte offset from the instruction's first row
@@ -238,7 +245,8 @@ struct DmaCopyT {
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
             const int r = (NW * i + w) * RPI + rl;
-            const int col = 32 * ((p >> 2) ^ bswT<R>(r & 3)) + 8 * (p & 3);
+            const int col = SW ? 16 * ((p >> 1) ^ fT16(r)) + 8 * (p & 1)
+                               : 32 * ((p >> 2) ^ bswT<R>(r & 3)) + 8 * (p & 3);
             voff[i] = (int)(rl * ldb2) + 2 * col;
             krow[i] = r;
         }

@@ -1,5 +1,5 @@
-// gba_kernel16.hpp -- the fast path on v_mfma_f32_16x16x32_f16 for operands
-// that are contiguous along the reduction (row-major A, column-major B).
+// gba_kernel16.hpp -- the fast path on v_mfma_f32_16x16x32_f16 (the 8-wave
+// tiles, every operand layout).
 //
 // Same decomposition as gemm_bias_act_fast (block tile per workgroup, warp
 // tiles per wave, 64-deep reduction steps through direct global -> LDS
@@ -18,7 +18,19 @@
 // order perm16: within each group of G blocks (16G columns), block t's MFMA
 // row rho is column 4G*(rho/4) + 4*(t%G) + rho%4, so across the group's G
 // blocks a lane holds 4G consecutive outputs of its row (16 for G = 4: two
-// 16-byte stores).
+// 16-byte stores).  An operand contiguous along N (row-major B) instead
+// uses G = 1, the natural column order: its transposing fragment reads then
+// touch 16 consecutive columns per row, which fT16 keeps free of bank
+// conflicts (the grouped order would put four 8-byte reads of a row into
+// four groups and conflict), and each lane stores 4 consecutive outputs.
+//
+// Layouts.  As in the 32x32 path each tile keeps its global layout in LDS:
+// reduction-contiguous operands as 128-byte rows (chunk permutations swzA16
+// / swzB16), M- or N-contiguous ones as 64 reduction rows whose 16-element
+// groups are permuted by fT16 of the row, read with ds_read_b64_tr_b16 pairs
+// (lanes 4j+c of a 16-lane group address row j at the 4-element chunk that
+// result lanes 4c..4c+3 need, so each lane receives 8 consecutive k of one
+// row or column, the same k slots as the 16-byte reads).
 //
 // Slices.  A 64-deep step is two 32-deep halves; each half is split into two
 // slices over the A blocks of the warp tile (TM/2 each), so a step has four
@@ -49,15 +61,17 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int TM = WTM / 16, TN = WTN / 16;   // 16x16 blocks of the warp tile
     constexpr int TMH = TM / 2;                    // A blocks per slice
-    constexpr int G = TN < 4 ? TN : 4;             // B blocks per group of consecutive outputs
+    // Operands contiguous along the reduction use DmaCopy and 16-byte
+    // fragment reads, the others (TA / TB) DmaCopyT and transposing reads.
+    constexpr bool TA = LA == COL, TB = LB == ROW;
+    constexpr int G = TB ? 1 : (TN < 4 ? TN : 4);  // B blocks per group of consecutive outputs
     constexpr int ROWB = BK * 2;                   // bytes per LDS row
     constexpr int SUB = (BM + BN) * ROWB;          // bytes per k-group sub-stage
     constexpr int STAGE = SK * SUB;                // bytes per LDS stage
     constexpr int NS = NSTG;
-    static_assert(LA == ROW && LB == COL, "16x16x32 path: reduction-contiguous operands");
     static_assert((NS & (NS - 1)) == 0, "stage count must be a power of two");
     static_assert(WTM % 32 == 0 && WTN % 32 == 0, "warp tile must be a multiple of 32x32");
-    static_assert(G >= 2 && TN % G == 0, "B blocks come in groups of two or four");
+    static_assert(TN % G == 0 && (TB || G >= 2), "B blocks come in groups of two or four");
     static_assert(!(ACC16 && SK > 1), "fp16 accumulation is defined for a single running sum");
     static_assert(!SPLIT || (SK == 1 && !ACC16), "a split reduction needs one k-group and fp32 sums");
     constexpr int PADN = BN + 4;               // fp32 row pitch of the split-K partial tiles
@@ -85,24 +99,39 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
     const int mc = m0 + BM <= p.M ? m0 : p.M - BM;
     const int nc = n0 + BN <= p.N ? n0 : p.N - BN;
 
-    using CopyA = DmaCopy<BM, NTG, 1>;
-    using CopyB = DmaCopy<BN, NTG, 2>;
+    using CopyA = std::conditional_t<TA, DmaCopyT<BM, NTG, 1>, DmaCopy<BM, NTG, 1>>;
+    using CopyB = std::conditional_t<TB, DmaCopyT<BN, NTG, 1>, DmaCopy<BN, NTG, 2>>;
     CopyA ca;
     CopyB cb;
 
     // Fragment byte offsets inside a stage, per 32-deep half h: A block s is
     // 16 rows (2048 bytes) after block 0 (swzA16 has period 16); each B
     // block has its own rows.
-    int offa[2], offb[2][TN];
+    int offa[TA ? TM : 2], offb[TB ? 1 : 2][TN];
     {
-        const int ra = wm * WTM + l16;
+        // transposing reads: lane 4j + c of group g4 addresses reduction row
+        // 8*g4 + j (+ 32 per half, + 4 for the second read of a pair) at the
+        // 4-element chunk 4c of the block's 16 elements
+        const int kr = 8 * g4 + (l16 >> 2), c4 = 4 * (l16 & 3);
+        if constexpr (TA) {
 #pragma unroll
-        for (int h = 0; h < 2; ++h) offa[h] = ra * ROWB + (((4 * h + g4) ^ swzA16(l16)) * 16);
+            for (int s = 0; s < TM; ++s)
+                offa[s] = kr * (2 * BM) + 32 * (((wm * WTM) / 16 + s) ^ fT16(kr)) + 2 * c4;
+        } else {
+            const int ra = wm * WTM + l16;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) offa[h] = ra * ROWB + (((4 * h + g4) ^ swzA16(l16)) * 16);
+        }
 #pragma unroll
         for (int t = 0; t < TN; ++t) {
-            const int rb = wn * WTN + perm16<G>(t, l16);
+            if constexpr (TB) {
+                offb[0][t] = BM * ROWB + kr * (2 * BN) + 32 * (((wn * WTN) / 16 + t) ^ fT16(kr)) + 2 * c4;
+            } else {
+                const int rb = wn * WTN + perm16<G>(t, l16);
 #pragma unroll
-            for (int h = 0; h < 2; ++h) offb[h][t] = (BM + rb) * ROWB + (((4 * h + g4) ^ swzB16(rb)) * 16);
+                for (int h = 0; h < 2; ++h)
+                    offb[h][t] = (BM + rb) * ROWB + (((4 * h + g4) ^ swzB16(rb)) * 16);
+            }
         }
     }
 
@@ -116,12 +145,17 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
     h8 fa[2][TMH], fb[2][TN];
     auto read_a = [&](int buf, const char *stage, int h, int q) {
 #pragma unroll
-        for (int s = 0; s < TMH; ++s)
-            fa[buf][s] = *reinterpret_cast<const h8 *>(stage + offa[h] + (q * TMH + s) * 16 * ROWB);
+        for (int s = 0; s < TMH; ++s) {
+            if constexpr (TA) fa[buf][s] = read_frag_tr<BM>(stage + offa[q * TMH + s] + h * 32 * (2 * BM));
+            else fa[buf][s] = *reinterpret_cast<const h8 *>(stage + offa[h] + (q * TMH + s) * 16 * ROWB);
+        }
     };
     auto read_b = [&](int buf, const char *stage, int h) {
 #pragma unroll
-        for (int t = 0; t < TN; ++t) fb[buf][t] = *reinterpret_cast<const h8 *>(stage + offb[h][t]);
+        for (int t = 0; t < TN; ++t) {
+            if constexpr (TB) fb[buf][t] = read_frag_tr<BN>(stage + offb[0][t] + h * 32 * (2 * BN));
+            else fb[buf][t] = *reinterpret_cast<const h8 *>(stage + offb[h][t]);
+        }
     };
     // The slice's MFMAs: A blocks q*TMH .. q*TMH+TMH-1 of half `bbuf`.
     auto mfmas = [&](int abuf, int bbuf, int q) {
@@ -160,7 +194,8 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
     };
 
     constexpr int NM = TN * TMH;              // MFMAs per slice
-    constexpr int NRA = TMH, NRB = TMH + TN;  // fragment reads of slices 0, 2 and of slices 1, 3
+    // fragment reads (DS instructions) of slices 0, 2 and of slices 1, 3
+    constexpr int NRA = TMH * (TA ? 2 : 1), NRB = NRA + TN * (TB ? 2 : 1);
     constexpr int NL = CopyA::NLOAD + CopyB::NLOAD;
     constexpr int VM_AT_BARRIER = (NS - 2) * NL;
     char *const mine = lds + grp * SUB;
@@ -168,14 +203,21 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
     // The row bias of this lane's output columns (4G consecutive per group
     // of G blocks), loaded before the reduction.
     constexpr int NGRP = TN / G;
-    h8 brow[SK == 1 ? NGRP : 1][G / 2];
+    constexpr int NV = G >= 2 ? G / 2 : 1;    // 8-element chunks per group (G = 1: one 4-element chunk)
+    h8 brow[SK == 1 ? NGRP : 1][NV];
     if constexpr (SK == 1) {
         if (p.bias_kind == BIAS_ROW) {
 #pragma unroll
             for (int tg = 0; tg < NGRP; ++tg) {
                 const _Float16 *bp = p.bias + nc + wn * WTN + 16 * G * tg + 4 * G * g4;
 #pragma unroll
-                for (int v = 0; v < G / 2; ++v) brow[tg][v] = *reinterpret_cast<const h8 *>(bp + 8 * v);
+                for (int v = 0; v < NV; ++v) {
+                    if constexpr (G >= 2) brow[tg][v] = *reinterpret_cast<const h8 *>(bp + 8 * v);
+                    else {
+                        const h4 b4 = *reinterpret_cast<const h4 *>(bp);
+                        brow[tg][v] = h8{b4[0], b4[1], b4[2], b4[3], 0, 0, 0, 0};
+                    }
+                }
             }
         }
     }
@@ -194,8 +236,14 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
         ca.init(ldx, gtid);
         cb.init(ldy, gtid);
 
-        auto rsrc_a = [&](int k0) { return make_rsrc(X + (int64_t)mc * ldx + k0, MAX_RECORDS); };
-        auto rsrc_b = [&](int k0) { return make_rsrc(Y + (int64_t)nc * ldy + k0, MAX_RECORDS); };
+        auto rsrc_a = [&](int k0) {
+            if constexpr (TA) return make_rsrc(X + (int64_t)k0 * ldx + mc, MAX_RECORDS);
+            else return make_rsrc(X + (int64_t)mc * ldx + k0, MAX_RECORDS);
+        };
+        auto rsrc_b = [&](int k0) {
+            if constexpr (TB) return make_rsrc(Y + (int64_t)k0 * ldy + nc, MAX_RECORDS);
+            else return make_rsrc(Y + (int64_t)nc * ldy + k0, MAX_RECORDS);
+        };
         const int nk_seg = (Kseg + SK * BK - 1) / (SK * BK);
         int s_lo = 0, s_hi = nk_seg;
         if constexpr (SPLIT) {
@@ -358,8 +406,9 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
 
     // Epilogue on registers: per A block and group of G B blocks a lane
     // holds 4G consecutive outputs of one row: +/- bias, activation, fp16,
-    // 16-byte stores (each guarded so an output shared with a neighbouring
-    // tile is stored by its owner only).  Row blocks outermost.
+    // 16-byte stores (8-byte for G = 1; each guarded so an output shared
+    // with a neighbouring tile is stored by its owner only).  Row blocks
+    // outermost.
 #pragma unroll
     for (int s = 0; s < TM; ++s) {
 #pragma unroll
@@ -371,29 +420,43 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
             for (int u = 0; u < G; ++u)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) x[4 * u + r] = acc[tg * G + u][s][r];
+            constexpr int W = G >= 2 ? 8 : 4;   // outputs per chunk
             if (p.bias_kind == BIAS_ROW) {
 #pragma unroll
-                for (int v = 0; v < G / 2; ++v)
+                for (int v = 0; v < NV; ++v)
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) x[8 * v + e] += p.bias_sign * (float)brow[tg][v][e];
+                    for (int e = 0; e < W; ++e) x[W * v + e] += p.bias_sign * (float)brow[tg][v][e];
             } else if (p.bias_kind == BIAS_FULL) {
                 const _Float16 *bp = p.bias + (int64_t)i * p.ldbias + j;
 #pragma unroll
-                for (int v = 0; v < G / 2; ++v) {
-                    const h8 bv = *reinterpret_cast<const h8 *>(bp + 8 * v);
+                for (int v = 0; v < NV; ++v) {
+                    if constexpr (W == 8) {
+                        const h8 bv = *reinterpret_cast<const h8 *>(bp + 8 * v);
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) x[8 * v + e] += p.bias_sign * (float)bv[e];
+                        for (int e = 0; e < 8; ++e) x[8 * v + e] += p.bias_sign * (float)bv[e];
+                    } else {
+                        const h4 bv = *reinterpret_cast<const h4 *>(bp);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) x[e] += p.bias_sign * (float)bv[e];
+                    }
                 }
             }
             activate(p.act, x);
             if (i >= m0) {
                 _Float16 *dst = p.C + (int64_t)i * p.ldc + j;
 #pragma unroll
-                for (int v = 0; v < G / 2; ++v) {
-                    h8 o;
+                for (int v = 0; v < NV; ++v) {
+                    if constexpr (W == 8) {
+                        h8 o;
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) o[e] = (_Float16)x[8 * v + e];
-                    if (j + 8 * v >= n0) *reinterpret_cast<h8 *>(dst + 8 * v) = o;
+                        for (int e = 0; e < 8; ++e) o[e] = (_Float16)x[8 * v + e];
+                        if (j + 8 * v >= n0) *reinterpret_cast<h8 *>(dst + 8 * v) = o;
+                    } else {
+                        h4 o;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) o[e] = (_Float16)x[e];
+                        if (j >= n0) *reinterpret_cast<h4 *>(dst) = o;
+                    }
                 }
             }
         }

@@ -74,11 +74,8 @@ struct LayoutTable {
 };
 
 // Which tiles run the 16x16x32 kernel (gemm_bias_act_fast16): the ones
-// with eight waves of one k-group.
-constexpr bool use_fast16(int la, int lb, int bm, int bn, int wm, int wn)
-{
-    return la == ROW && lb == COL && bm >= 128 && bn >= 128 && wm * wn == 8;
-}
+// with eight waves of one k-group, in every layout.
+constexpr bool use_fast16(int bm, int bn, int wm, int wn) { return bm >= 128 && bn >= 128 && wm * wn == 8; }
 
 template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool PRO, bool DUAL,
           bool SPLIT = false>
@@ -86,12 +83,11 @@ hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
 {
     // one workgroup per output tile, times the splits of its reduction
     dim3 grid((unsigned)(a.tiles_m * a.tiles_n * (SPLIT ? a.splits : 1))), block(64 * WM * WN * SK);
-    // The 8-wave tiles (one k-group) with reduction-contiguous operands run
-    // on 16x16x32 MFMAs, everything else
+    // The 8-wave tiles (one k-group) run on 16x16x32 MFMAs, everything else
     // on 32x32x16 (measured per tile: the 16x16x32 kernels of the 4-wave
     // tiles were up to 20% slower, and the 4-wave 256x256 one does not fit
     // its 64 accumulator blocks per wave in registers)
-    if constexpr (use_fast16(LA, LB, BM, BN, WM, WN))
+    if constexpr (use_fast16(BM, BN, WM, WN))
         hipLaunchKernelGGL((gemm_bias_act_fast16<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, PRO, DUAL, SPLIT>), grid,
                            block, 0, s, a);
     else
