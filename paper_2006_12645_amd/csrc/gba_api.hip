@@ -85,12 +85,15 @@ int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum);
 //     makes at most 128 workgroups, else by 32x64 with four k-groups when
 //     that makes at most 256 -- then 32x32.
 // The 256x128 and 128x256 tiles (4 or 8 waves) were never clearly the
-// fastest in those sweeps and are only used when asked for.  With
-// reduction-contiguous operands and fp32 accumulation, 128x128 means the
-// 8-wave tile on 16x16x32 MFMAs (3-6% faster than the 4-wave one over the
-// shapes the rule gives it; over two sweeps of random shapes the rule is
-// then 0.8-0.9% slower in total than the per-shape best tile).
-int select_tile(int64_t M, int64_t N, int64_t K, int accum, bool rc)
+// fastest in those sweeps and are only used when asked for.  128x128 means
+// the 8-wave tile on 16x16x32 MFMAs: with fp32 accumulation 3-6% faster
+// than the 4-wave one over the shapes the rule gives it (over two sweeps of
+// random shapes the rule is then 0.8-0.9% slower in total than the
+// per-shape best tile in the RC layout), except with column-major A and
+// row-major B, where the two were within a few percent either way; with
+// fp16 accumulation 25-40% faster in every layout (two waves per SIMD
+// overlap one wave's rounding with the other's MFMAs).
+int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb)
 {
     auto tiles = [&](int t) -> int64_t {
         return tile_fits(t, M, N) ? ceil_div(M, TILES[t].bm) * ceil_div(N, TILES[t].bn) : 0;
@@ -98,7 +101,8 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum, bool rc)
     if (tiles(1) >= 136) return 1;
     if (tiles(1) >= 112 && tiles(4) > 512) return 1;  // 128x128 would need a second round
     const int t = select_tile_rest(M, N, K, accum);
-    return rc && accum == GBA_ACC_F32 && t == 4 ? 18 : t;
+    const bool cr = la == GBA_COL_MAJOR && lb == GBA_ROW_MAJOR;
+    return t == 4 && (accum == GBA_ACC_F16 || !cr) ? 18 : t;
 }
 
 // The rule below the 256x256 cases.
@@ -213,8 +217,8 @@ Plan make_plan(const gba_fused_desc &d, bool may_split)
     const bool fp32 = d.accum == GBA_ACC_F32;
     int64_t auto_s = 1;
     if (may_split && d.split_k == 0 && !tile_ok && fp32) auto_s = auto_splits(d.M, d.N, ktot);
-    pl.tile = tile_ok ? d.tile_id : (auto_s > 1 ? AUTO_SPLIT_TILE : select_tile(d.M, d.N, ktot, d.accum,
-                                                                                  d.layoutA == GBA_ROW_MAJOR && d.layoutB == GBA_COL_MAJOR));
+    pl.tile = tile_ok ? d.tile_id
+                      : (auto_s > 1 ? AUTO_SPLIT_TILE : select_tile(d.M, d.N, ktot, d.accum, d.layoutA, d.layoutB));
     if (pl.tile >= 0 && !fast_path_ok(d)) pl.tile = -1;
     pl.cfg = pl.tile >= 0 ? TILES[pl.tile] : GENERIC_TILE;
     pl.tiles_m = ceil_div(d.M, pl.cfg.bm);
@@ -486,7 +490,7 @@ extern "C" int gba_select_tile(gba_layout layoutA, gba_layout layoutB, int64_t M
     if (!is_layout(layoutA) || !is_layout(layoutB)) return -1;
     if (accum != GBA_ACC_F32 && accum != GBA_ACC_F16) return -1;
     if (M < 0 || N < 0 || K < 0 || M > INT_MAX || N > INT_MAX || K > INT_MAX) return -1;
-    return select_tile(M, N, K, accum, layoutA == GBA_ROW_MAJOR && layoutB == GBA_COL_MAJOR);  // -1 also when the general path would run
+    return select_tile(M, N, K, accum, layoutA, layoutB);  // -1 also when the general path would run
 }
 
 extern "C" gba_status gba_bias_add_f16(int64_t M, int64_t N, void *C, int64_t ldc, const void *bias,
