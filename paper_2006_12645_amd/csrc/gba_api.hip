@@ -90,9 +90,10 @@ int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum);
 // than the 4-wave one over the shapes the rule gives it (over two sweeps of
 // random shapes the rule is then 0.8-0.9% slower in total than the
 // per-shape best tile in the RC layout), except with column-major A and
-// row-major B, where the two were within a few percent either way; with
-// fp16 accumulation 25-40% faster in every layout (two waves per SIMD
-// overlap one wave's rounding with the other's MFMAs).
+// row-major B, where the two were within a few percent either way.  With
+// fp16 accumulation the 8-wave tiles are 25-40% faster than the 4-wave
+// ones from 128x128 down and about 10% faster than 64x64 or 32x64 on the
+// small-M inference shapes (measured in the RC layout), so they come first.
 int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb)
 {
     auto tiles = [&](int t) -> int64_t {
@@ -100,6 +101,14 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb)
     };
     if (tiles(1) >= 136) return 1;
     if (tiles(1) >= 112 && tiles(4) > 512) return 1;  // 128x128 would need a second round
+    if (accum == GBA_ACC_F16) {
+        // fp16 accumulation: the 8-wave tiles on 16x16x32 MFMAs (their two
+        // waves per SIMD overlap one wave's rounding with the other's
+        // MFMAs), 128x128 from 128 workgroups, else 128x64 or 64x128
+        if (tiles(18) >= 128) return 18;
+        if (tile_fits(19, M, N) && lb == GBA_COL_MAJOR) return 19;
+        if (tile_fits(20, M, N) && la == GBA_ROW_MAJOR) return 20;
+    }
     const int t = select_tile_rest(M, N, K, accum);
     const bool cr = la == GBA_COL_MAJOR && lb == GBA_ROW_MAJOR;
     return t == 4 && (accum == GBA_ACC_F16 || !cr) ? 18 : t;

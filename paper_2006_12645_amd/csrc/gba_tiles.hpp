@@ -45,9 +45,11 @@ struct TileCfg {
     X(15, 64, 128, 1, 2, 2, 2)   \
     X(16, 256, 128, 2, 4, 1, 2)  \
     X(17, 128, 256, 4, 2, 1, 2)  \
-    X(18, 128, 128, 2, 4, 1, 2)
+    X(18, 128, 128, 2, 4, 1, 2)  \
+    X(19, 128, 64, 4, 2, 1, 2)   \
+    X(20, 64, 128, 2, 4, 1, 2)
 
-constexpr int NUM_TILES = 19;
+constexpr int NUM_TILES = 21;
 
 #define GBA_TILE_CFG(id, BM, BN, WM, WN, SK, NSTG) TileCfg{BM, BN, WM, WN, SK, NSTG},
 constexpr TileCfg TILES[NUM_TILES] = {GBA_TILE_LIST(GBA_TILE_CFG)};
@@ -74,8 +76,13 @@ struct LayoutTable {
 };
 
 // Which tiles run the 16x16x32 kernel (gemm_bias_act_fast16): the ones
-// with eight waves of one k-group, in every layout.
-constexpr bool use_fast16(int bm, int bn, int wm, int wn) { return bm >= 128 && bn >= 128 && wm * wn == 8; }
+// with eight waves of one k-group, in every layout where an M- or
+// N-contiguous operand tile has 128 or more elements per row (its
+// conflict-free group permutation needs eight 16-element groups).
+constexpr bool use_fast16(int la, int lb, int bm, int bn, int wm, int wn)
+{
+    return wm * wn == 8 && (bm >= 128 || la == ROW) && (bn >= 128 || lb == COL);
+}
 
 template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool PRO, bool DUAL,
           bool SPLIT = false>
@@ -87,7 +94,7 @@ hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
     // on 32x32x16 (measured per tile: the 16x16x32 kernels of the 4-wave
     // tiles were up to 20% slower, and the 4-wave 256x256 one does not fit
     // its 64 accumulator blocks per wave in registers)
-    if constexpr (use_fast16(BM, BN, WM, WN))
+    if constexpr (use_fast16(LA, LB, BM, BN, WM, WN))
         hipLaunchKernelGGL((gemm_bias_act_fast16<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, PRO, DUAL, SPLIT>), grid,
                            block, 0, s, a);
     else
