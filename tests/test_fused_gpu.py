@@ -252,6 +252,23 @@ def test_headline_tile_integer_exact(accum):
         assert np.array_equal(got, ref), (kw, np.abs(got - ref).max())
 
 
+# Large shapes on the 8-wave tiles: more output tiles than compute units (two
+# or more rounds of workgroups), ragged edges and a K tail; the oracle checks
+# sampled rows.
+
+@pytest.mark.parametrize("tile,M,N", [(1, 4168, 5160), (16, 4104, 4136), (17, 4104, 4136),
+                                      (18, 4168, 3112), (19, 4168, 3112), (20, 4168, 3112)])
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_large_shapes_on_eight_wave_tiles(tile, M, N, layout):
+    announce("large 8-wave", tile, layout, M, N)
+    pr = Problem(790 + tile, M, N, 200, full_bias=tile % 2 == 0)
+    kw = dict(prologue=tile % 3 == 0, bias_op="sub" if tile % 2 else "add", act="relu")
+    rows = sorted({0, 1, 127, 128, 255, 256, M // 2, M - 73, M - 1} |
+                  set(int(r) for r in np.random.default_rng(tile).integers(0, M, 12)))
+    got = pr.gpu(layout, tile=tile, **kw)[rows]
+    U.assert_close(got, pr.oracle(rows=rows, **kw), what=f"tile {tile} {layout}")
+
+
 @pytest.mark.parametrize("tile", [4, 10, 13, 14])
 def test_integer_exact_split_k(tile):
     announce("integer_splitk", tile)
