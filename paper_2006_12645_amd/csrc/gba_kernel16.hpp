@@ -198,6 +198,13 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
     constexpr int NRA = TMH * (TA ? 2 : 1), NRB = NRA + TN * (TB ? 2 : 1);
     constexpr int NL = CopyA::NLOAD + CopyB::NLOAD;
     constexpr int VM_AT_BARRIER = (NS - 2) * NL;
+    // Tiles that put two workgroups on a compute unit (by their LDS) raise
+    // their waves' priority over the first three slices of a step (the
+    // MFMA-only stretch), so a workgroup there is not held back by the
+    // copies and barrier of the other: 2-5% on the 8-wave 128x128 tile; it
+    // made the 256x256 tile (one workgroup per compute unit) 1-2% slower and
+    // the 128x64 one (three) no faster, which do not use it.
+    constexpr bool PRIO = NS * STAGE <= 80 * 1024 && NS * STAGE > 160 * 1024 / 3;
     char *const mine = lds + grp * SUB;
 
     // The row bias of this lane's output columns (4G consecutive per group
@@ -282,6 +289,7 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
             char *nxt = mine + ((kt + 1) & (NS - 1)) * STAGE;
             // slice 0: half 0, first A blocks
             read_a(1, cur, 0, 1);
+            if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
             mfmas(0, 0, 0);
             sched_slice<NM, NRA, 0, 0, false>();
             // slice 1: half 0, second A blocks (B fragments of half 1 in flight)
@@ -294,6 +302,7 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
             read_a(1, cur, 1, 1);
             mfmas(0, 1, 0);
             sched_slice<NM, NRA, 0, 0, false>();
+            if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
             // Step kt+1 complete in LDS for every wave; every read of `cur` done.
             if constexpr (VM_AT_BARRIER == 0) {
                 __builtin_amdgcn_s_waitcnt(0);
