@@ -348,7 +348,7 @@ def counters_zero(ws, tile, M, N):
     return not ws[:tiles * 4].any().item()
 
 
-@pytest.mark.parametrize("tile", [4, 5, 6, 7, 8, 9, 18])
+@pytest.mark.parametrize("tile", [4, 5, 6, 7, 8, 9, 18, 19, 20])
 @pytest.mark.parametrize("split", [2, 3, 7])
 def test_split_reduction_all_features(tile, split):
     # 16 + 4 steps of A.B and P.Q, ragged output (shifted edge tiles)
