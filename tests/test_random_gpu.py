@@ -2,7 +2,9 @@
 combination of layout, tile (or the library's choice), prologue, second
 product, bias kind and sign, activation, accumulation, reduction split and
 operand alignment, on seeded random shapes that mostly are not multiples of
-the tiles.  Each case prints its parameters before touching the GPU.
+the tiles.  A second sweep puts every request on one of the 8-wave tiles at
+shapes from the tile's size up to ~700 more.  Each case prints its
+parameters before touching the GPU.
 """
 import numpy as np
 import pytest
@@ -17,7 +19,8 @@ torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
 ACT = {"none": O.ACT_NONE, "relu": O.ACT_RELU, "sigmoid": O.ACT_SIGMOID, "tanh": O.ACT_TANH}
-NUM_CASES = 64
+NUM_CASES = 256
+NUM_CASES_EIGHT_WAVE = 64
 
 
 def draw(seed):
@@ -56,9 +59,33 @@ def operand(x, lay, offset):
     return t[:, :cols] if lay == D.ROW else t[:, :rows].t()
 
 
+def draw_eight_wave(seed):
+    """A request on one of the 8-wave tiles (the 16x16x32 kernel in most
+    layouts), with every dimension at least the tile's and up to ~700 more."""
+    c = draw(100000 + seed)
+    rng = np.random.default_rng(777000 + seed)
+    t = int(rng.choice([1, 16, 17, 18, 19, 20]))
+    info = gba.tile_info(t)
+    mult = 8 if rng.random() < 0.8 else 1
+    c["M"] = info["bm"] + int(rng.integers(0, 700)) // mult * mult + (0 if mult == 8 else int(rng.integers(1, 8)))
+    c["N"] = info["bn"] + int(rng.integers(0, 700)) // 8 * 8
+    c["tile"] = t
+    if c["split"] is not None and info["bm"] * info["bn"] > 128 * 128:
+        c["split"] = None
+    return c
+
+
 @pytest.mark.parametrize("seed", range(NUM_CASES))
 def test_random_request(seed):
-    c = draw(seed)
+    run_case(seed, draw(seed))
+
+
+@pytest.mark.parametrize("seed", range(NUM_CASES_EIGHT_WAVE))
+def test_random_request_eight_wave_tiles(seed):
+    run_case(100000 + seed, draw_eight_wave(seed))
+
+
+def run_case(seed, c):
     print("CASE", seed, c, flush=True)
     M, N, K = c["M"], c["N"], c["K"]
     A, B, _ = D.random_problem(91000 + seed, M, N, K)
