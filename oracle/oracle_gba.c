@@ -14,7 +14,10 @@
  *     out(i,j) = act == RELU ? (pre > 0 ? pre : 0) : pre
  *
  * evaluated in IEEE binary64 with k ascending, the bias added last, and no
- * rounding to fp16 anywhere.  Inputs are fp16 bit patterns decoded by the
+ * rounding to fp16 anywhere.  (The one exception is the fp16-accumulation
+ * reading offered by oracle_fused_rows_f64 with acc16 = 1, described above
+ * product_row_acc16: one running sum through both products, rounded to
+ * binary16 at the end of every aligned 32-deep group of each product.)  Inputs are fp16 bit patterns decoded by the
  * routine below (sign, 5-bit exponent, 10-bit fraction, subnormals).  The
  * product of two fp16 values is exact in binary64 (11 + 11 significant bits),
  * so the only rounding is in the running sum.

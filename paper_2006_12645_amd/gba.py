@@ -182,18 +182,41 @@ def workspace_size(desc):
 
 # Zero-filled workspaces, one per (device, stream): the library leaves the
 # counters at their start zero after every call, so a workspace stays ready
-# for the next call in that stream's order.
+# for the next call in that stream's order.  A workspace that is replaced by
+# a larger one is kept alive (in _retired), since a graph captured earlier
+# may still hold its address.
 _workspaces = {}
+_retired = []
+
+
+def stream_capturing(stream):
+    """True while `stream` is being captured into a HIP graph."""
+    import torch
+    with torch.cuda.stream(stream):
+        return torch.cuda.is_current_stream_capturing()
 
 
 def stream_workspace(nbytes, device, stream=None):
-    """A zero-filled uint8 CUDA tensor of at least nbytes for calls on `stream`."""
+    """A zero-filled uint8 CUDA tensor of at least nbytes for calls on `stream`.
+
+    Allocating and zero-filling it is itself GPU work on `stream`, so it is
+    refused while the stream is being captured into a graph: make one eager
+    call first (the cached workspace is then reused during capture), or pass
+    a caller-owned zero-filled workspace.
+    """
     import torch
     if stream is None:
         stream = torch.cuda.current_stream(device)
     key = (torch.device(device).index, stream.cuda_stream)
     ws = _workspaces.get(key)
     if ws is None or ws.numel() < nbytes:
+        if stream_capturing(stream):
+            raise RuntimeError(
+                f"workspace='auto' would allocate and zero-fill {nbytes} bytes while the stream is "
+                "being captured into a graph; pass a zero-filled uint8 CUDA tensor of at least that "
+                "size as `workspace`, or make one call before the capture")
+        if ws is not None:
+            _retired.append(ws)
         with torch.cuda.stream(stream):
             ws = torch.zeros(max(nbytes, 1 << 20), dtype=torch.uint8, device=device)
         _workspaces[key] = ws

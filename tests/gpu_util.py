@@ -36,13 +36,17 @@ def oracle_for(A, B, bias, act=O.ACT_RELU, rows=None):
 def assert_close(gpu_f16, ref, accum="f32", what=""):
     g = np.asarray(gpu_f16, dtype=np.float64)
     atol, rtol = TOL[accum]
+    if g.shape != np.shape(ref):
+        raise AssertionError(f"{what}: shape {g.shape} against the oracle's {np.shape(ref)}")
     err = np.abs(g - ref)
     bound = atol + rtol * np.abs(ref)
-    bad = err > bound
+    # written as "not within" so that a NaN or infinite output (for which
+    # every comparison is false) counts as a mismatch
+    bad = ~(err <= bound)
     if bad.any():
         idx = np.argwhere(bad)[:5]
         raise AssertionError(
             f"{what}: {int(bad.sum())} of {bad.size} outside |d| <= {atol} + {rtol}|ref|; "
-            f"max err {err.max():.4g}; first at {idx.tolist()}: gpu {g[tuple(idx[0])]} ref "
-            f"{ref[tuple(idx[0])]}")
+            f"max err {np.nanmax(np.where(np.isfinite(err), err, np.inf)):.4g}; first at {idx.tolist()}: "
+            f"gpu {g[tuple(idx[0])]} ref {ref[tuple(idx[0])]}")
     return float(err.max())

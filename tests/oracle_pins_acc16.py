@@ -6,6 +6,8 @@ Like oracle_pins.py: each ``pin_*`` takes an opened oracle library and
 raises AssertionError when the library disagrees with a fact fixed by the
 IEEE 754 format, by exact rational arithmetic or by a closed form.
 """
+import json
+import os
 from fractions import Fraction
 
 import numpy as np
@@ -14,6 +16,7 @@ from oracle import oracle as O
 from paper_2006_12645_amd import datagen as D
 
 KC = 32
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
 
 def f16(x):
@@ -133,5 +136,42 @@ def pin_acc16_integer_data_is_exact(lib):
     assert np.array_equal(got, exact)
 
 
+def golden_row(spec, K):
+    """A 1 x K fp16 row from a golden case's sparse spec: keys are an index
+    "k" or a range "lo:hi", values the fp16 value stored there."""
+    row = np.zeros((1, K), np.float16)
+    for key, v in spec.items():
+        lo, _, hi = key.partition(":")
+        row[0, int(lo):int(hi) if hi else int(lo) + 1] = v
+    return row
+
+
+def golden_acc16_sum_of_products():
+    with open(os.path.join(GOLDEN, "acc16_sum_of_products.json")) as f:
+        return json.load(f)["cases"]
+
+
+def pin_acc16_sum_of_products_golden(lib):
+    """Hand-derived binary16 results of the single running sum through A.B
+    and then P.Q (tests/golden/acc16_sum_of_products.json): cancellation
+    into a lower binade, a rounding inside P.Q's group, and groups aligned
+    per product.  Each case is chosen so that two separate accumulators
+    (Listing 5's C and R) give a different value; the binary64 path must
+    give the exact one."""
+    for case in golden_acc16_sum_of_products():
+        K, K2 = case["K"], case["K2"]
+        a, p = golden_row(case["A"], K), golden_row(case["P"], K2)
+        b, q = np.ones((K, 1), np.float16), np.ones((K2, 1), np.float16)
+        for la in (D.ROW, D.COL):
+            for lb in (D.ROW, D.COL):
+                kw = dict(second=case["second"], p_store=D.store(p, la), q_store=D.store(q, lb), K2=K2,
+                          act=O.ACT_NONE, nthreads=1, lib=lib)
+                got = O.fused(D.store(a, la), la, D.store(b, lb), lb, 1, 1, K, acc16=True, **kw)
+                assert got[0, 0] == case["one_sum"], (case["name"], la, lb, got[0, 0])
+                assert case["one_sum"] != case["two_sums"]
+                ex = O.fused(D.store(a, la), la, D.store(b, lb), lb, 1, 1, K, **kw)
+                assert ex[0, 0] == case["exact"], (case["name"], la, lb, ex[0, 0])
+
+
 PINS = [pin_round_f16_vs_numpy, pin_acc16_single_group, pin_acc16_group_rounding_closed_form,
-        pin_acc16_brute_force, pin_acc16_integer_data_is_exact]
+        pin_acc16_brute_force, pin_acc16_integer_data_is_exact, pin_acc16_sum_of_products_golden]

@@ -337,3 +337,29 @@ def test_add_validation():
     assert L.gba_add_f16(4, 4, FAKE, 4, FAKE, 3, None) == gba.GBA_EINVAL
     assert L.gba_add_f16(4, 4, FAKE, 4, FAKE + 1, 4, None) == gba.GBA_EUNSUPPORTED
     assert L.gba_add_f16(0, 4, None, 4, None, 4, None) == gba.GBA_OK
+
+
+class _FakeStream:
+    cuda_stream = 0x1234
+
+
+def test_auto_workspace_refused_during_capture(monkeypatch):
+    """workspace='auto' must not allocate or zero-fill a buffer while the
+    stream is being captured into a graph (that work would be captured)."""
+    from paper_2006_12645_amd import gba
+    monkeypatch.setattr(gba, "_workspaces", {})
+    monkeypatch.setattr(gba, "stream_capturing", lambda s: True)
+    with pytest.raises(RuntimeError, match="captured"):
+        gba.stream_workspace(1 << 20, "cuda:0", _FakeStream())
+
+
+def test_auto_workspace_reused_during_capture(monkeypatch):
+    """A workspace cached by an earlier eager call is handed out during
+    capture without any new allocation, and a replaced one is kept alive."""
+    from paper_2006_12645_amd import gba
+    cached = type("T", (), {"numel": lambda self: 4 << 20})()
+    monkeypatch.setattr(gba, "_workspaces", {(0, _FakeStream.cuda_stream): cached})
+    monkeypatch.setattr(gba, "stream_capturing", lambda s: True)
+    assert gba.stream_workspace(1 << 20, "cuda:0", _FakeStream()) is cached
+    with pytest.raises(RuntimeError):
+        gba.stream_workspace(8 << 20, "cuda:0", _FakeStream())

@@ -212,6 +212,43 @@ def test_fp16_accumulation_matches_its_emulation(tile, layout):
     assert close.mean() >= 0.99, close.mean()
 
 
+@pytest.mark.parametrize("tile", [None, 1, 4, 6, 9, 18, 19, 20, "general"])
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_fp16_accumulation_sum_of_products_golden(tile, layout):
+    """The hand-derived binary16 results of the single running sum through
+    A.B and then P.Q (tests/golden/acc16_sum_of_products.json), chosen so
+    that two separate accumulators would give another value.  Each golden
+    row of A and P sits in the first and last row of a 264x264 problem and B
+    and Q have ones in the first and last column, so the four corner outputs
+    carry the golden value (including shifted edge tiles) and every other
+    output is 0."""
+    import oracle_pins_acc16 as PA
+    M = N = 264
+    for case in PA.golden_acc16_sum_of_products():
+        announce("f16acc golden", case["name"], tile, layout)
+        K, K2 = case["K"], case["K2"]
+        pr = Problem(0, M, N, K, K2=K2, bias=None)
+        pr.A, pr.P = np.zeros((M, K), np.float16), np.zeros((M, K2), np.float16)
+        pr.B, pr.Q = np.zeros((K, N), np.float16), np.zeros((K2, N), np.float16)
+        for r in (0, M - 1):
+            pr.A[r] = PA.golden_row(case["A"], K)[0]
+            pr.P[r] = PA.golden_row(case["P"], K2)[0]
+        for c in (0, N - 1):
+            pr.B[:, c] = 1
+            pr.Q[:, c] = 1
+        second = "add" if case["second"] > 0 else "sub"
+        kw = dict(second=second, act="none", accum="f16")
+        if tile == "general":
+            got = pr.gpu(layout, offset=True, **kw)
+        else:
+            got = pr.gpu(layout, tile=tile, **kw)
+        want = np.zeros((M, N))
+        for r in (0, M - 1):
+            for c in (0, N - 1):
+                want[r, c] = case["one_sum"]
+        assert np.array_equal(got.astype(np.float64), want), (case["name"], got[0, 0], got[-1, -1])
+
+
 # ----------------------------------------------------------------------------
 # Integer data: every partial sum is a small integer, so results are exact
 
@@ -253,8 +290,8 @@ def test_headline_tile_integer_exact(accum):
 
 
 # Large shapes on the 8-wave tiles: more output tiles than compute units (two
-# or more rounds of workgroups), ragged edges and a K tail; the oracle checks
-# sampled rows.
+# or more rounds of workgroups), ragged edges and a K tail; every output
+# against the oracle.
 
 @pytest.mark.parametrize("tile,M,N", [(1, 4168, 5160), (16, 4104, 4136), (17, 4104, 4136),
                                       (18, 4168, 3112), (19, 4168, 3112), (20, 4168, 3112)])
@@ -263,10 +300,8 @@ def test_large_shapes_on_eight_wave_tiles(tile, M, N, layout):
     announce("large 8-wave", tile, layout, M, N)
     pr = Problem(790 + tile, M, N, 200, full_bias=tile % 2 == 0)
     kw = dict(prologue=tile % 3 == 0, bias_op="sub" if tile % 2 else "add", act="relu")
-    rows = sorted({0, 1, 127, 128, 255, 256, M // 2, M - 73, M - 1} |
-                  set(int(r) for r in np.random.default_rng(tile).integers(0, M, 12)))
-    got = pr.gpu(layout, tile=tile, **kw)[rows]
-    U.assert_close(got, pr.oracle(rows=rows, **kw), what=f"tile {tile} {layout}")
+    got = pr.gpu(layout, tile=tile, **kw)
+    U.assert_close(got, pr.oracle(**kw), what=f"tile {tile} {layout}")
 
 
 @pytest.mark.parametrize("tile", [4, 10, 13, 14])
@@ -455,39 +490,36 @@ def test_deterministic():
         assert np.array_equal(pr.gpu("RC", **kw), first)
 
 
-def test_sum4096_sampled_rows():
-    """The sum-of-products workload at full size (4096^3 twice), checked on
-    sampled rows, in the launch the benchmark times."""
+def test_sum4096_full():
+    """The sum-of-products workload at full size (4096^3 twice), every output
+    against the oracle, in the launch the benchmark times."""
     w = D.WORKLOADS["sum4096_RC"]
-    announce(w.name)
+    announce(w.name, "every output")
     A, B, bias = D.logical_inputs(w)
     P, Q = D.second_inputs(w)
-    rows = sorted({0, 1, 255, 256, 2047, 4095} | set(int(r) for r in
-                                                      np.random.default_rng(5).integers(0, w.M, 10)))
     dA = U.device_operand(A, D.ROW)
     dB = U.device_operand(B, D.COL)
     dP = U.device_operand(P, D.ROW)
     dQ = U.device_operand(Q, D.COL)
     out = gba.fused_gemm(dA, dB, P=dP, Q=dQ, bias=torch.from_numpy(bias).cuda(), act="relu")
     torch.cuda.synchronize()
-    got = out.cpu().numpy()[rows]
+    got = out.cpu().numpy()
     ref = O.fused(D.store(A, D.ROW), D.ROW, D.store(B, D.COL), D.COL, w.M, w.N, w.K, second=1,
                   p_store=D.store(P, D.ROW), q_store=D.store(Q, D.COL), K2=w.extra["K2"], bias=bias,
-                  act=O.ACT_RELU, rows=rows)
+                  act=O.ACT_RELU)
     U.assert_close(got, ref, what=w.name)
 
 
-def test_prologue4096_sampled_rows():
+def test_prologue4096_full():
     w = D.WORKLOADS["prologue4096_RC"]
-    announce(w.name)
+    announce(w.name, "every output")
     A, B, bias = D.logical_inputs(w)
-    rows = sorted({0, 255, 256, 4095} | set(int(r) for r in np.random.default_rng(6).integers(0, w.M, 10)))
     out = gba.fused_gemm(U.device_operand(A, D.ROW), U.device_operand(B, D.COL), prologue="relu",
                          bias=torch.from_numpy(bias).cuda(), act="relu")
     torch.cuda.synchronize()
     ref = O.fused(D.store(A, D.ROW), D.ROW, D.store(B, D.COL), D.COL, w.M, w.N, w.K,
-                  prologue_relu=True, bias=bias, act=O.ACT_RELU, rows=rows)
-    U.assert_close(out.cpu().numpy()[rows], ref, what=w.name)
+                  prologue_relu=True, bias=bias, act=O.ACT_RELU)
+    U.assert_close(out.cpu().numpy(), ref, what=w.name)
 
 
 def test_unfused_add_piece():

@@ -75,6 +75,12 @@ MUTANTS += [
     ("acc16_no_tail_rounding", "if (k % 32 == 31 || k == K - 1)", "if (k % 32 == 31)"),
     ("acc16_round_only_at_end", "if (k % 32 == 31 || k == K - 1)", "if (k == K - 1)"),
     ("acc16_second_not_subtracted", "J->second > 0 ? 1.0 : -1.0);", "1.0);"),
+    # Listing 5's two accumulators instead of the one running sum: P.Q
+    # accumulated (and rounded) on its own, then added in binary64
+    ("acc16_two_accumulators",
+     "product_row_acc16(J, J->P, J->ldp, J->Qd, J->K2, i, c, J->second > 0 ? 1.0 : -1.0);",
+     "{ product_row_acc16(J, J->P, J->ldp, J->Qd, J->K2, i, r, J->second > 0 ? 1.0 : -1.0);\n"
+     "                  for (int64_t j = 0; j < J->N; ++j) c[j] = c[j] + r[j]; }"),
 ]
 
 ALL_PINS = P.PINS + PF.PINS + PA.PINS

@@ -35,15 +35,6 @@ def run_gpu(A, B, bias, layout, act="relu", accum="f32", tile=None, pad=0, out=N
     return o
 
 
-def sample_rows(M, seed, count=24):
-    rng = np.random.default_rng(seed)
-    rows = {0, M - 1, M // 2}
-    for edge in (128, 256):
-        rows.update(r for r in (edge - 1, edge, M - edge) if 0 <= r < M)
-    rows.update(int(r) for r in rng.integers(0, M, size=count))
-    return sorted(rows)
-
-
 @pytest.fixture(autouse=True, scope="module")
 def _gpu():
     if not torch.cuda.is_available():
@@ -79,44 +70,46 @@ def test_cube1024_layouts(cube1024, layout):
 
 @pytest.fixture(scope="module")
 def cube4096():
+    """The 4096^3 headline inputs and the oracle over EVERY output: the fused
+    result (bias + ReLU) and the plain product (no bias, no activation)."""
     w = D.WORKLOADS["cube4096_RC"]
     A, B, bias = D.logical_inputs(w)
-    rows = sample_rows(w.M, 4096)
-    return A, B, bias, rows
+    ref_fused = U.oracle_for(A, B, bias)
+    ref_plain = U.oracle_for(A, B, None, act=O.ACT_NONE)
+    return A, B, bias, ref_fused, ref_plain
 
 
-def test_cube4096_fused_sampled(cube4096):
-    A, B, bias, rows = cube4096
-    announce("cube4096 fused RC rows", len(rows))
-    got = run_gpu(A, B, bias, "RC").cpu().numpy()[rows]
-    U.assert_close(got, U.oracle_for(A, B, bias, rows=rows), what="4096^3 fused")
+def test_cube4096_fused_full(cube4096):
+    A, B, bias, ref, _ = cube4096
+    announce("cube4096 fused RC, every output")
+    got = run_gpu(A, B, bias, "RC").cpu().numpy()
+    U.assert_close(got, ref, what="4096^3 fused")
 
 
-def test_cube4096_plain_sampled(cube4096):
-    A, B, _, rows = cube4096
-    announce("cube4096 plain RC")
-    got = run_gpu(A, B, None, "RC", act="none").cpu().numpy()[rows]
-    U.assert_close(got, U.oracle_for(A, B, None, act=O.ACT_NONE, rows=rows), what="4096^3 plain")
+def test_cube4096_plain_full(cube4096):
+    A, B, _, _, ref = cube4096
+    announce("cube4096 plain RC, every output")
+    got = run_gpu(A, B, None, "RC", act="none").cpu().numpy()
+    U.assert_close(got, ref, what="4096^3 plain")
 
 
-def test_cube4096_unfused_sampled(cube4096):
-    A, B, bias, rows = cube4096
-    announce("cube4096 unfused RC")
+def test_cube4096_unfused_full(cube4096):
+    A, B, bias, ref, _ = cube4096
+    announce("cube4096 unfused RC, every output")
     dA = U.device_operand(A, D.ROW)
     dB = U.device_operand(B, D.COL)
     out = gba.unfused_gemm_bias_relu(dA, dB, torch.from_numpy(bias).cuda())
     torch.cuda.synchronize()
-    U.assert_close(out.cpu().numpy()[rows], U.oracle_for(A, B, bias, rows=rows), what="unfused")
+    U.assert_close(out.cpu().numpy(), ref, what="unfused")
 
 
 @pytest.mark.parametrize("name", ["mlp_up_8192x4096x1024", "mlp_down_8192x1024x4096"])
-def test_mlp_sampled(name):
+def test_mlp_full(name):
     w = D.WORKLOADS[name]
-    announce(name)
+    announce(name, "every output")
     A, B, bias = D.logical_inputs(w)
-    rows = sample_rows(w.M, w.seed_base)
-    got = run_gpu(A, B, bias, "RC").cpu().numpy()[rows]
-    U.assert_close(got, U.oracle_for(A, B, bias, rows=rows), what=name)
+    got = run_gpu(A, B, bias, "RC").cpu().numpy()
+    U.assert_close(got, U.oracle_for(A, B, bias), what=name)
 
 
 @pytest.mark.parametrize("name", ["infer_m32_n4096_k1024", "infer_m128_n4096_k1024",
