@@ -19,6 +19,8 @@
  *     the GPU that is current for `stream`).  fp16 means IEEE binary16.
  *   - The caller owns every buffer.  The library never allocates, frees or
  *     synchronises; it keeps no mutable global state and is thread-safe.
+ *     The one exception is gba_fused_gemm_noalloc, which uses a static
+ *     device array of the library's own (see there).
  *   - Calls are asynchronous: work is enqueued on `stream` (NULL = the null
  *     stream) and the function returns once the kernel is launched.
  *   - Arguments are validated on the host before anything is enqueued.  On
@@ -30,6 +32,7 @@
 #ifndef GBA_H
 #define GBA_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -48,7 +51,9 @@ typedef enum {
     GBA_OK = 0,
     GBA_EINVAL = 1,        /* malformed argument (negative size, ld too small, NULL, bad enum) */
     GBA_EUNSUPPORTED = 2,  /* well-formed but outside what the library implements */
-    GBA_EHIP = 3           /* the HIP runtime reported an error at launch */
+    GBA_EHIP = 3,          /* the HIP runtime reported an error at launch */
+    GBA_ESCRATCH = 4       /* gba_fused_gemm_noalloc: the request needs more scratch than
+                              GBA_NOALLOC_SCRATCH_BYTES */
 } gba_status;
 
 /*
@@ -230,6 +235,34 @@ gba_status gba_fused_workspace_size(const gba_fused_desc *desc, size_t *bytes);
  * aligned; GBA_EHIP if the launch fails.  Nothing is launched on error.
  */
 gba_status gba_fused_gemm(const gba_fused_desc *desc, gba_stream_t stream);
+
+/*
+ * gba_fused_gemm_noalloc -- gba_fused_gemm for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same request, same result bits as
+ * gba_fused_gemm given a workspace of at least gba_fused_workspace_size
+ * bytes; desc->workspace and desc->workspace_bytes are ignored.
+ *
+ * When the request splits its reduction across workgroups, the split's
+ * workspace is the library's own static device array of
+ * GBA_NOALLOC_SCRATCH_BYTES bytes (one per GPU, created with the library's
+ * code object and held until the process ends); its counters are cleared by
+ * a small kernel on `stream` before the split kernel.  Requests that do not
+ * split use no scratch.  The call allocates nothing (no hipMalloc, no
+ * allocating library routine); its first call on a device looks up that
+ * device's scratch address once, with the device current.
+ *
+ * Every call on one GPU shares that GPU's scratch, which keeps the last
+ * call's contents: calls that may overlap on one GPU (different streams,
+ * different host threads without ordering) race on it and give undefined
+ * results.  Calls in one stream's order are safe.
+ *
+ * Errors: as gba_fused_gemm; GBA_ESCRATCH (nothing launched) when the split
+ * the request asks for (or the library chooses) needs more than
+ * GBA_NOALLOC_SCRATCH_BYTES; GBA_EUNSUPPORTED for a device index >= 64.
+ */
+#define GBA_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+gba_status gba_fused_gemm_noalloc(const gba_fused_desc *desc, gba_stream_t stream);
 
 /* Number of tile configurations compiled into the library. */
 int gba_num_tiles(void);

@@ -4,6 +4,8 @@
 #include <limits.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "gba.h"
 #include "gba_tiles.hpp"
 
@@ -423,6 +425,50 @@ gba_status validate_pointwise(int64_t M, int64_t N, const void *C, int64_t ldc, 
     return GBA_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Library-held scratch of gba_fused_gemm_noalloc: the workspace of a
+// reduction split across workgroups (per-tile arrival counters, then the
+// fp32 partial tiles), for callers that cannot allocate.  One copy per GPU,
+// at its own device address, held until the process ends.  In host code
+// the array's name is only a host-side stand-in: kernels and copies get the
+// device address from hipGetSymbolAddress, taken once per device.
+
+constexpr size_t NOALLOC_SCRATCH_BYTES = GBA_NOALLOC_SCRATCH_BYTES;
+static_assert(NOALLOC_SCRATCH_BYTES % 256 == 0, "scratch size keeps 256-byte alignment");
+
+static __device__ __align__(256) char scratch[NOALLOC_SCRATCH_BYTES];
+
+constexpr int MAX_DEVICES = 64;
+std::once_flag scratch_once[MAX_DEVICES];
+void *scratch_ptr[MAX_DEVICES];
+hipError_t scratch_err[MAX_DEVICES];
+
+// Device address of the current device's scratch (looked up on the first
+// call per device, with that device current).
+gba_status device_scratch(void **ptr)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return GBA_EHIP;
+    if (dev < 0 || dev >= MAX_DEVICES) return GBA_EUNSUPPORTED;
+    std::call_once(scratch_once[dev], [dev] {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        scratch_err[dev] = e;
+        scratch_ptr[dev] = e == hipSuccess ? p : nullptr;
+    });
+    if (scratch_err[dev] != hipSuccess || scratch_ptr[dev] == nullptr) return GBA_EHIP;
+    *ptr = scratch_ptr[dev];
+    return GBA_OK;
+}
+
+// Sets n 32-bit words to zero: the split counters are cleared with a kernel
+// (a memset node in a captured graph is not reliable on this platform).
+__global__ void __launch_bounds__(256) zero_words_kernel(unsigned *p, int n)
+{
+    const int i = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+    if (i < n) p[i] = 0u;
+}
+
 }  // namespace
 }  // namespace gba
 
@@ -457,6 +503,33 @@ extern "C" gba_status gba_fused_gemm(const gba_fused_desc *desc, gba_stream_t st
 {
     if (desc == nullptr) return GBA_EINVAL;
     return run_fused(*desc, reinterpret_cast<hipStream_t>(stream));
+}
+
+extern "C" gba_status gba_fused_gemm_noalloc(const gba_fused_desc *desc, gba_stream_t stream)
+{
+    if (desc == nullptr) return GBA_EINVAL;
+    gba_fused_desc d = *desc;
+    d.workspace = nullptr;  // the caller's workspace fields are ignored
+    d.workspace_bytes = 0;
+    gba_status st = validate(d);
+    if (st != GBA_OK || d.M == 0 || d.N == 0) return st;
+    const Plan pl = make_plan(d, true);
+    if (pl.splits > 1) {
+        if (pl.ws_bytes > NOALLOC_SCRATCH_BYTES) return GBA_ESCRATCH;
+        void *ws = nullptr;
+        st = device_scratch(&ws);
+        if (st != GBA_OK) return st;
+        // The counters must be zero when the split kernel starts, whatever an
+        // earlier call left behind.
+        const int64_t ntiles = pl.tiles_m * pl.tiles_n;
+        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        hipLaunchKernelGGL(zero_words_kernel, dim3((unsigned)ceil_div(ntiles, 256)), dim3(256), 0, s,
+                           static_cast<unsigned *>(ws), (int)ntiles);
+        if (hipGetLastError() != hipSuccess) return GBA_EHIP;
+        d.workspace = ws;
+        d.workspace_bytes = NOALLOC_SCRATCH_BYTES;
+    }
+    return run_fused(d, reinterpret_cast<hipStream_t>(stream));
 }
 
 extern "C" gba_status gemm_bias_act(gba_layout layoutA, gba_layout layoutB, int64_t M, int64_t N,
@@ -559,6 +632,9 @@ extern "C" const char *gba_status_string(gba_status status)
     case GBA_EINVAL: return "GBA_EINVAL: invalid argument";
     case GBA_EUNSUPPORTED: return "GBA_EUNSUPPORTED: unsupported argument";
     case GBA_EHIP: return "GBA_EHIP: HIP launch error";
+    case GBA_ESCRATCH:
+        return "GBA_ESCRATCH: the request's split reduction needs more than the library's static "
+               "scratch (GBA_NOALLOC_SCRATCH_BYTES); use gba_fused_gemm with a workspace or fewer splits";
     }
     return "unknown gba_status";
 }

@@ -15,7 +15,8 @@ LIB_PATH = os.path.join(PKG, "libgba.so")
 GBA_ROW_MAJOR, GBA_COL_MAJOR = 0, 1
 GBA_ACT_NONE, GBA_ACT_RELU, GBA_ACT_SIGMOID, GBA_ACT_TANH = 0, 1, 2, 3
 GBA_ACC_F32, GBA_ACC_F16 = 0, 1
-GBA_OK, GBA_EINVAL, GBA_EUNSUPPORTED, GBA_EHIP = 0, 1, 2, 3
+GBA_OK, GBA_EINVAL, GBA_EUNSUPPORTED, GBA_EHIP, GBA_ESCRATCH = 0, 1, 2, 3, 4
+GBA_NOALLOC_SCRATCH_BYTES = 16 << 20
 GBA_PRO_NONE, GBA_PRO_RELU = 0, 1
 GBA_SECOND_NONE, GBA_SECOND_ADD, GBA_SECOND_SUB = 0, 1, 2
 GBA_BIAS_NONE, GBA_BIAS_ROW, GBA_BIAS_FULL = 0, 1, 2
@@ -53,6 +54,7 @@ SIGNATURES = {
     "gba_add_f16": (_int, [_i64, _i64, _vp, _i64, _vp, _i64, _vp]),
     "gba_fused_desc_init": (None, [ctypes.POINTER(FusedDesc)]),
     "gba_fused_gemm": (_int, [ctypes.POINTER(FusedDesc), _vp]),
+    "gba_fused_gemm_noalloc": (_int, [ctypes.POINTER(FusedDesc), _vp]),
     "gba_fused_workspace_size": (_int, [ctypes.POINTER(FusedDesc), ctypes.POINTER(ctypes.c_size_t)]),
     "gba_status_string": (_cp, [_int]),
     "gba_version": (_cp, []),
@@ -173,6 +175,14 @@ def fused_gemm_desc(desc, stream=None, device=None):
     _check(lib().gba_fused_gemm(ctypes.byref(desc), _stream_handle(stream, device)), "gba_fused_gemm")
 
 
+def fused_gemm_desc_noalloc(desc, stream=None, device=None):
+    """Launch gba_fused_gemm_noalloc on a filled FusedDesc: a split reduction
+    uses the library's static scratch, nothing is allocated (raises on
+    error)."""
+    _check(lib().gba_fused_gemm_noalloc(ctypes.byref(desc), _stream_handle(stream, device)),
+           "gba_fused_gemm_noalloc")
+
+
 def workspace_size(desc):
     """Bytes of workspace a filled FusedDesc would use to split its reduction."""
     n = ctypes.c_size_t(0)
@@ -236,7 +246,9 @@ def fused_gemm(A, B, *, P=None, Q=None, second="add", prologue=None, bias=None, 
     fp16, allocated when None.  split: None (library's choice) or the number
     of workgroups each output tile's reduction is split across (1: never).
     workspace: "auto" (a cached zero-filled buffer for this stream), None
-    (no split), or a zero-filled uint8 CUDA tensor owned by the caller.
+    (no split), a zero-filled uint8 CUDA tensor owned by the caller, or
+    "static" (gba_fused_gemm_noalloc: the library's own static scratch,
+    nothing allocated).
     """
     import torch
     M, K = A.shape
@@ -296,6 +308,9 @@ def fused_gemm(A, B, *, P=None, Q=None, second="add", prologue=None, bias=None, 
     d.C, d.ldc = out.data_ptr(), _row_major_ld(out, "out")
     d.tile_id = -1 if tile is None else int(tile)
     d.split_k = 0 if split is None else int(split)
+    if isinstance(workspace, str) and workspace == "static":
+        fused_gemm_desc_noalloc(d, stream, A.device)
+        return out
     if workspace is not None:
         need = workspace_size(d)
         if need > 0:

@@ -135,7 +135,7 @@ def test_select_tile_rejects_bad_input():
 
 
 def test_status_strings_and_version():
-    for s in range(4):
+    for s in range(5):
         assert gba.lib().gba_status_string(s)
     assert b"unknown" in gba.lib().gba_status_string(99)
     assert "gfx950" in gba.version()
@@ -363,3 +363,22 @@ def test_auto_workspace_reused_during_capture(monkeypatch):
     assert gba.stream_workspace(1 << 20, "cuda:0", _FakeStream()) is cached
     with pytest.raises(RuntimeError):
         gba.stream_workspace(8 << 20, "cuda:0", _FakeStream())
+
+
+def test_noalloc_rejects_a_split_beyond_its_scratch():
+    """gba_fused_gemm_noalloc refuses, before any launch, a split whose
+    workspace exceeds the library's static scratch; it validates like
+    gba_fused_gemm."""
+    L = gba.lib()
+    d = gba.new_desc()
+    d.layoutA, d.layoutB = gba.GBA_ROW_MAJOR, gba.GBA_COL_MAJOR
+    d.M, d.N, d.K = 1024, 1024, 8192
+    d.A = d.B = d.C = FAKE
+    d.lda, d.ldb, d.ldc = 8192, 8192, 1024
+    d.tile_id, d.split_k = 4, 64          # 64 tiles of 128x128, 64 splits each
+    assert gba.workspace_size(d) > gba.GBA_NOALLOC_SCRATCH_BYTES
+    assert L.gba_fused_gemm_noalloc(ctypes.byref(d), None) == gba.GBA_ESCRATCH
+    assert b"scratch" in L.gba_status_string(gba.GBA_ESCRATCH)
+    d.M = -1
+    assert L.gba_fused_gemm_noalloc(ctypes.byref(d), None) == gba.GBA_EINVAL
+    assert L.gba_fused_gemm_noalloc(None, None) == gba.GBA_EINVAL
