@@ -5,9 +5,15 @@ Default workload: M = N = K = 4096, A row-major, B column-major, fp16
 uniform[-1,1] inputs, fp32 accumulation, bias + ReLU epilogue.  A step is one
 call of the fused kernel; the metric is 2MNK / time in TFLOP/s.
 
-Prints ONE JSON line (see the keys below).  Besides the headline it reports
-the unfused three-launch chain (GEMM, bias add, ReLU) and the plain GEMM on
-the same inputs, the roofline position of the fused kernel, and the CPU
+Prints ONE JSON line.  `value` and `ms_per_step` come from K fused launches
+back to back (HIP events around the K launches on the stream the library
+launches on).  The comparison legs -- the fused kernel again, the plain GEMM,
+the unfused three-launch chain (GEMM, bias add, ReLU), the two-launch chain
+(GEMM, then bias add + ReLU in one pass) and torch's library path -- are then
+timed interleaved: K rounds, one launch of every leg per round, each launch
+between its own pair of events, so clock and power drift fall on every leg
+alike; each leg reports its median and mean, and the speedups use medians.
+The line also carries the fused kernel's roofline position and the CPU
 oracle timed on a bounded sample of the same problem.
 
 --workload prologue4096_RC times relu(A).B + bias -> ReLU (against a ReLU
@@ -18,6 +24,7 @@ and a ReLU); their metric counts 2MN(K + K2) flops.
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--tile ID]
                     [--report PATH] [--no-cpu]
     python bench.py --configs      # every workload configuration, one line each
+    python bench.py --sweep [N]    # the paper's protocol: N random sizes
 """
 import argparse
 import hashlib
@@ -78,8 +85,32 @@ def time_launches(fn, steps, warmup, torch):
     return start.elapsed_time(stop) / steps
 
 
+def cpu_share():
+    """Threads the oracle may use on this host: every CPU this process may run
+    on, capped by OMP_NUM_THREADS when that is set (the CPU share of a GPU
+    box), and the host facts reported beside the figure."""
+    try:
+        visible = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        visible = os.cpu_count() or 1
+    cap = os.environ.get("OMP_NUM_THREADS")
+    threads = min(visible, int(cap)) if cap and cap.isdigit() and int(cap) > 0 else visible
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return threads, visible, os.cpu_count(), model
+
+
 def cpu_baseline(w, A, B, bias, P=None, Q=None, target_s=12.0):
-    """The oracle on a bounded sample of output rows of the same problem."""
+    """The oracle on a bounded sample of output rows of the same problem, on
+    every thread of this process's CPU share, plus a single-thread run on the
+    1000^3 problem (rows of the ragged workload) for a per-core rate."""
     from oracle import oracle as O
     from paper_2006_12645_amd import datagen as D
     a_st, b_st = D.store(A, D.ROW), D.store(B, D.COL)
@@ -87,11 +118,11 @@ def cpu_baseline(w, A, B, bias, P=None, Q=None, target_s=12.0):
     kw = dict(prologue_relu=w.extra.get("prologue") == "relu", bias=bias, act=O.ACT_RELU)
     if P is not None:
         kw.update(second=1, p_store=D.store(P, D.ROW), q_store=D.store(Q, D.COL), K2=K2)
-    threads = O.default_threads()
+    threads, visible, host_cpus, model = cpu_share()
 
-    def run(rows):
+    def run(rows, nthreads=threads):
         t0 = time.perf_counter()
-        O.fused(a_st, D.ROW, b_st, D.COL, w.M, w.N, w.K, rows=rows, nthreads=threads, **kw)
+        O.fused(a_st, D.ROW, b_st, D.COL, w.M, w.N, w.K, rows=rows, nthreads=nthreads, **kw)
         return time.perf_counter() - t0
 
     rows = list(range(min(w.M, 4 * threads)))
@@ -100,37 +131,52 @@ def cpu_baseline(w, A, B, bias, P=None, Q=None, target_s=12.0):
     nrows = int(min(w.M, max(len(rows), len(rows) * target_s / max(dt, 1e-3))))
     dt = run(list(range(nrows)))
     flops = 2.0 * nrows * w.N * (w.K + K2)
+    # one thread on the ragged 1000^3 problem: a per-core rate
+    r = D.WORKLOADS["ragged1000"]
+    rA, rB, rbias = D.logical_inputs(r)
+    r_rows = list(range(r.M))
+    t0 = time.perf_counter()
+    O.gemm_bias_act(D.store(rA, D.ROW), D.ROW, D.store(rB, D.COL), D.COL, r.M, r.N, r.K, bias=rbias,
+                    act=O.ACT_RELU, rows=r_rows, nthreads=1)
+    dt1 = time.perf_counter() - t0
+    per_core = 2.0 * len(r_rows) * r.N * r.K / dt1 / 1e9
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "sample": f"{nrows} of {w.M} output rows (all {w.N} columns, full reduction "
                       f"K={w.K}{f' + K2={K2}' if K2 else ''}) of the same {w.name} problem, "
-                      f"fp64, {dt:.1f} s"}
+                      f"fp64, {dt:.1f} s on {threads} threads",
+            "threads": threads, "host_cpus_visible": visible, "host_cpus": host_cpus,
+            "cpu_model": model,
+            "single_thread": {"GFLOP/s": round(per_core, 3),
+                              "sample": f"{len(r_rows)} of 1000 output rows of the 1000^3 ragged "
+                                        f"problem, 1 thread, {dt1:.2f} s"}}
 
 
-def time_graph(fns, launches, replays, torch):
-    """Average ms per launch of `launches` calls (cycling through fns)
-    captured in one HIP graph and replayed: device time without the host's
-    per-call launch cost."""
-    side = torch.cuda.Stream()
-    side.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(side):
-        for f in fns[:3]:
-            f()
-    torch.cuda.current_stream().wait_stream(side)
+def time_interleaved(legs, rounds, warmup, torch):
+    """Per-launch times (ms) of every leg, interleaved: `rounds` rounds, each
+    launching every leg once in turn, each launch between its own pair of
+    events on the current stream (where the library launches).  Returns
+    {name: {"median_ms", "mean_ms"}}."""
+    names = list(legs)
+    for _ in range(warmup):
+        for n in names:
+            legs[n]()
     torch.cuda.synchronize()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
-        for i in range(launches):
-            fns[i % len(fns)]()
-    g.replay()
+    ev = {n: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(rounds)] for n in names}
+    for r in range(rounds):
+        for n in names:
+            a, b = ev[n][r]
+            a.record()
+            legs[n]()
+            b.record()
     torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    start.record()
-    for _ in range(replays):
-        g.replay()
-    stop.record()
-    torch.cuda.synchronize()
-    return start.elapsed_time(stop) / (replays * launches)
+    out = {}
+    for n in names:
+        t = sorted(a.elapsed_time(b) for a, b in ev[n])
+        mid = len(t) // 2
+        med = t[mid] if len(t) % 2 else 0.5 * (t[mid - 1] + t[mid])
+        out[n] = {"median_ms": round(med, 5), "mean_ms": round(sum(t) / len(t), 5)}
+    return out
 
 
 COLD_POOL_BYTES = 1 << 30
@@ -153,14 +199,67 @@ def cold_operands(torch, dA, dB, M, N, nsets):
     return list(zip(pool(dA), pool(dB), [outs[i] for i in range(nsets)]))
 
 
+def graph_legs(legs, launches, rounds, torch):
+    """Median ms per launch of every leg: each leg's `launches` calls (cycling
+    through its list of callables) captured in one HIP graph, then `rounds`
+    rounds replaying every leg's graph once in turn, each replay between its
+    own pair of events (interleaved, so drift falls on every leg alike)."""
+    graphs = {}
+    for name, fns in legs.items():
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for f in fns[:3]:
+                f()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(launches):
+                fns[i % len(fns)]()
+        g.replay()
+        graphs[name] = g
+    torch.cuda.synchronize()
+    ev = {n: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(rounds)] for n in graphs}
+    for r in range(rounds):
+        for n, g in graphs.items():
+            a, b = ev[n][r]
+            a.record()
+            g.replay()
+            b.record()
+    torch.cuda.synchronize()
+    out = {}
+    for n in graphs:
+        t = sorted(a.elapsed_time(b) / launches for a, b in ev[n])
+        mid = len(t) // 2
+        out[n] = t[mid] if len(t) % 2 else 0.5 * (t[mid - 1] + t[mid])
+    del graphs
+    return out
+
+
+def chain_legs(gba, dA, dB, dbias, out, acc="f32", tile=None):
+    """The fused call and the two unfused chains on the same operands."""
+    return {
+        "fused": lambda: gba.gemm_bias_act(dA, dB, dbias, act="relu", accum=acc, out=out, tile=tile),
+        "chain3": lambda: (gba.gemm_bias_act(dA, dB, None, act="none", accum=acc, out=out, tile=tile),
+                           gba.bias_add_(out, dbias), gba.relu_(out)),
+        "chain2": lambda: (gba.gemm_bias_act(dA, dB, None, act="none", accum=acc, out=out, tile=tile),
+                           gba.bias_act_(out, dbias, "relu")),
+    }
+
+
 def configs(args, np, torch, D, gba):
     """Every single-product workload configuration: layouts x accumulations,
     the library's tile choice.  `us` is device time per launch from a
     captured graph of back-to-back launches on the same (cache-resident)
-    operands; `us_eager` the same launches issued one by one from Python.
-    The roofline bound is HBM below the ridge point (peak flops / peak
-    bytes) and MFMA above it; HBM-bound rows also give a cold-cache figure
-    (`cold`), rotating through at least 1 GiB of operand copies."""
+    operands, timed interleaved with the two unfused chains on the same
+    operands (`chain3_us`: GEMM, bias add, ReLU; `chain2_us`: GEMM, then bias
+    add and ReLU in one pass) and their speedups; `us_eager` the fused
+    launches issued one by one from Python.  The roofline bound is HBM below
+    the ridge point (peak flops / peak bytes) and MFMA above it; HBM-bound
+    rows also give cold-cache figures (`cold`), rotating through at least
+    1 GiB of operand copies, for the fused kernel and both chains."""
     ridge = PEAK_F16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
     for w in D.WORKLOADS.values():
         if w.extra:
@@ -178,9 +277,16 @@ def configs(args, np, torch, D, gba):
             dB = (torch.from_numpy(B).cuda() if lb == D.ROW
                   else torch.from_numpy(np.ascontiguousarray(B.T)).cuda().t())
             for acc in w.accum:
-                call = lambda a, b, c: (lambda: gba.gemm_bias_act(a, b, dbias, act="relu", accum=acc, out=c))
-                ms_eager = time_launches(call(dA, dB, out), args.steps, args.warmup, torch)
-                ms = time_graph([call(dA, dB, out)], args.steps, 10, torch)
+                legs = chain_legs(gba, dA, dB, dbias, out, acc)
+                ms_eager = time_launches(legs["fused"], args.steps, args.warmup, torch)
+                if args.fused_only:
+                    # eager fused launches only (for counter runs of the profiler)
+                    print(json.dumps({"workload": w.name, "M": w.M, "N": w.N, "K": w.K, "layout": layout,
+                                      "accum": acc, "tile": gba.select_tile(w.M, w.N, w.K, la, lb, acc),
+                                      "us_eager": round(ms_eager * 1e3, 2)}), flush=True)
+                    continue
+                t = graph_legs({k: [f] for k, f in legs.items()}, args.steps, 10, torch)
+                ms = t["fused"]
                 tf = flops / (ms * 1e-3) / 1e12
                 gbs = nbytes / (ms * 1e-3) / 1e9
                 line = {
@@ -189,16 +295,66 @@ def configs(args, np, torch, D, gba):
                     "us_eager": round(ms_eager * 1e3, 2), "TFLOP/s": round(tf, 1), "GB/s": round(gbs, 1),
                     "roofline": {"bound": "hbm" if hbm else "mfma",
                                  "frac": round(gbs / PEAK_HBM_GBS if hbm else tf / PEAK_F16_TFLOPS, 4)},
+                    "chain3_us": round(t["chain3"] * 1e3, 2), "chain2_us": round(t["chain2"] * 1e3, 2),
+                    "speedup_vs_chain3": round(t["chain3"] / ms, 3),
+                    "speedup_vs_chain2": round(t["chain2"] / ms, 3),
                 }
                 if hbm:
                     nsets = -(-COLD_POOL_BYTES // int(nbytes))
                     sets = cold_operands(torch, dA, dB, w.M, w.N, nsets)
-                    ms_cold = time_graph([call(*s) for s in sets], nsets, 3, torch)
-                    del sets
-                    gbs_cold = nbytes / (ms_cold * 1e-3) / 1e9
-                    line["cold"] = {"us": round(ms_cold * 1e3, 2), "GB/s": round(gbs_cold, 1),
-                                    "frac": round(gbs_cold / PEAK_HBM_GBS, 4), "sets": nsets}
+                    cold_legs = {}
+                    for k in ("fused", "chain3", "chain2"):
+                        cold_legs[k] = [chain_legs(gba, a, b, dbias, c, acc)[k] for a, b, c in sets]
+                    tc = graph_legs(cold_legs, nsets, 3, torch)
+                    del sets, cold_legs
+                    gbs_cold = nbytes / (tc["fused"] * 1e-3) / 1e9
+                    line["cold"] = {"us": round(tc["fused"] * 1e3, 2), "GB/s": round(gbs_cold, 1),
+                                    "frac": round(gbs_cold / PEAK_HBM_GBS, 4), "sets": nsets,
+                                    "chain3_us": round(tc["chain3"] * 1e3, 2),
+                                    "chain2_us": round(tc["chain2"] * 1e3, 2),
+                                    "speedup_vs_chain3": round(tc["chain3"] / tc["fused"], 3),
+                                    "speedup_vs_chain2": round(tc["chain2"] / tc["fused"], 3)}
                 print(json.dumps(line), flush=True)
+
+
+def sweep(args, np, torch, D, gba):
+    """The paper's evaluation protocol on MI355X: random problem sizes, each a
+    multiple of 128 up to 4096 (datagen.sweep_shapes), RC layout, fp32
+    accumulation, uniform[-1,1] data; per size the fused kernel (library tile
+    choice) against the unfused three-launch chain (the paper's baseline:
+    GEMM, bias add, ReLU), the two-launch chain and, as context, torch's
+    library path (hipBLASLt GEMM, then add and ReLU), all graph-timed and
+    interleaved.  One JSON line per size, then a summary line: sizes where
+    fused wins, peak, worst, geometric and arithmetic mean speedup."""
+    import math
+    shapes = D.sweep_shapes(count=args.sweep)
+    rows = []
+    for idx, (M, N, K) in enumerate(shapes):
+        A, B, bias = D.random_problem(900000 + 10 * idx, M, N, K)
+        dA = torch.from_numpy(A).cuda()
+        dB = torch.from_numpy(np.ascontiguousarray(B.T)).cuda().t()
+        dbias = torch.from_numpy(bias).cuda()
+        out = torch.empty((M, N), dtype=torch.float16, device="cuda")
+        legs = chain_legs(gba, dA, dB, dbias, out)
+        legs["library_chain"] = lambda: (torch.matmul(dA, dB, out=out), out.add_(dbias), out.relu_())
+        t = graph_legs({k: [f] for k, f in legs.items()}, 10, 5, torch)
+        line = {"M": M, "N": N, "K": K, "tile": gba.select_tile(M, N, K),
+                "fused_us": round(t["fused"] * 1e3, 2),
+                "TFLOP/s": round(2.0 * M * N * K / (t["fused"] * 1e-3) / 1e12, 1),
+                **{f"{k}_us": round(t[k] * 1e3, 2) for k in ("chain3", "chain2", "library_chain")},
+                **{f"speedup_vs_{k}": round(t[k] / t["fused"], 3) for k in ("chain3", "chain2",
+                                                                            "library_chain")}}
+        rows.append(line)
+        print(json.dumps(line), flush=True)
+        del dA, dB, out
+    summary = {"sweep": f"{len(rows)} random sizes, multiples of 128 up to 4096, RC, fp32 accumulation, "
+                        "GEMM+bias+ReLU"}
+    for k in ("chain3", "chain2", "library_chain"):
+        sp = [r[f"speedup_vs_{k}"] for r in rows]
+        summary[k] = {"wins": sum(1 for x in sp if x > 1.0), "of": len(sp), "peak": max(sp),
+                      "worst": min(sp), "geomean": round(math.exp(sum(map(math.log, sp)) / len(sp)), 3),
+                      "mean": round(sum(sp) / len(sp), 3)}
+    print(json.dumps(summary), flush=True)
 
 
 def main():
@@ -218,7 +374,10 @@ def main():
     ap.add_argument("--configs", action="store_true",
                     help="instead of the headline line: one JSON line per workload "
                          "configuration (every layout and accumulation it lists) with its "
-                         "roofline position")
+                         "roofline position and fused-vs-unfused speedups")
+    ap.add_argument("--sweep", type=int, nargs="?", const=100, default=0, metavar="N",
+                    help="instead of the headline line: the paper's protocol over N random "
+                         "sizes (default 100), one line per size and a summary line")
     args = ap.parse_args()
 
     if args.calibrate_copy:
@@ -247,6 +406,9 @@ def main():
     if args.configs:
         configs(args, np, torch, D, gba)
         return
+    if args.sweep:
+        sweep(args, np, torch, D, gba)
+        return
     w = D.WORKLOADS[args.workload]
     A, B, bias = D.logical_inputs(w)
     dA = torch.from_numpy(A).cuda()                                    # row-major
@@ -263,48 +425,46 @@ def main():
         dQ = torch.from_numpy(np.ascontiguousarray(Q.T)).cuda().t()
     tile = args.tile if args.tile is not None else gba.select_tile(w.M, w.N, w.K + K2)
 
+    # the comparison legs, timed interleaved after the headline window
+    legs = {}
     if prologue is None and P is None:
-        # the headline: gemm_bias_act, and the paper's unfused three-launch chain
+        # the headline: gemm_bias_act, the plain GEMM, the paper's unfused
+        # three-launch chain and the two-launch variant
         fused = lambda: gba.gemm_bias_act(dA, dB, dbias, act="relu", out=out, tile=tile)
-        plain = lambda: gba.gemm_bias_act(dA, dB, None, act="none", out=out, tile=tile)
-        unfused = lambda: gba.unfused_gemm_bias_relu(dA, dB, dbias, out=out, tile=tile)
+        legs["plain"] = lambda: gba.gemm_bias_act(dA, dB, None, act="none", out=out, tile=tile)
+        legs["unfused_chain"] = lambda: gba.unfused_gemm_bias_relu(dA, dB, dbias, out=out, tile=tile)
+        legs["unfused_chain2"] = lambda: gba.unfused_gemm_bias_relu_2(dA, dB, dbias, out=out, tile=tile)
         idiom = "GEMM+bias+ReLU"
         chain = "GEMM, bias add, ReLU"
+        chain2 = "GEMM, then bias add and ReLU in one pass"
         plain_leg = "GEMM only (no bias, no activation)"
-
         # context: the same problem through torch's library path (hipBLASLt
         # GEMM, torch's elementwise kernels), the counterpart of the paper's
         # library baseline
-        def lib_chain():
-            torch.matmul(dA, dB, out=out)
-            out.add_(dbias)
-            out.relu_()
-
-        def lib_addmm_relu():
-            torch.addmm(dbias, dA, dB, out=out)
-            out.relu_()
-        library = {"library_gemm": lambda: torch.matmul(dA, dB, out=out),
-                   "library_chain": lib_chain, "library_addmm_relu": lib_addmm_relu}
+        legs["library_gemm"] = lambda: torch.matmul(dA, dB, out=out)
+        legs["library_chain"] = lambda: (torch.matmul(dA, dB, out=out), out.add_(dbias), out.relu_())
+        legs["library_addmm_relu"] = lambda: (torch.addmm(dbias, dA, dB, out=out), out.relu_())
     elif P is None:
         # relu(A).B + bias -> ReLU; unfused: ReLU pass over A, then the fused GEMM
         a_relu = dA.clone()
         fused = lambda: gba.fused_gemm(dA, dB, prologue="relu", bias=dbias, act="relu", out=out,
                                        tile=tile)
-        plain = lambda: gba.gemm_bias_act(dA, dB, dbias, act="relu", out=out, tile=tile)
+        legs["plain"] = lambda: gba.gemm_bias_act(dA, dB, dbias, act="relu", out=out, tile=tile)
 
         def unfused():
             gba.relu_(a_relu)
             gba.gemm_bias_act(a_relu, dB, dbias, act="relu", out=out, tile=tile)
+        legs["unfused_chain"] = unfused
         idiom = "ReLU-prologue GEMM+bias+ReLU"
-        library = {}
         chain = "ReLU over A, GEMM+bias+ReLU"
+        chain2 = None
         plain_leg = "GEMM+bias+ReLU without the prologue"
     else:
         # A.B + P.Q + bias -> ReLU; unfused: two GEMMs, add, bias add, ReLU
         tmp = torch.empty_like(out)
         fused = lambda: gba.fused_gemm(dA, dB, P=dP, Q=dQ, bias=dbias, act="relu", out=out,
                                        tile=tile)
-        plain = lambda: gba.gemm_bias_act(dA, dB, dbias, act="relu", out=out, tile=tile)
+        legs["plain"] = lambda: gba.gemm_bias_act(dA, dB, dbias, act="relu", out=out, tile=tile)
 
         def unfused():
             gba.gemm_bias_act(dA, dB, None, act="none", out=out, tile=tile)
@@ -312,25 +472,30 @@ def main():
             gba.add_(out, tmp)
             gba.bias_add_(out, dbias)
             gba.relu_(out)
+
+        def unfused2():
+            gba.gemm_bias_act(dA, dB, None, act="none", out=out, tile=tile)
+            gba.gemm_bias_act(dP, dQ, None, act="none", out=tmp, tile=tile)
+            gba.add_(out, tmp)
+            gba.bias_act_(out, dbias, "relu")
+        legs["unfused_chain"] = unfused
+        legs["unfused_chain2"] = unfused2
         idiom = "Add(GEMM,GEMM)+bias+ReLU"
-        library = {}
         chain = "GEMM, GEMM, add, bias add, ReLU"
+        chain2 = "GEMM, GEMM, add, then bias add and ReLU in one pass"
         plain_leg = "GEMM+bias+ReLU of A.B alone"
 
+    # The comparison legs first (interleaved), then the headline window:
+    # `warmup` untimed and `steps` timed fused launches back to back, on a
+    # GPU that is already running (not ramping up from idle).
+    inter = {}
+    if args.fused_only:
+        args.no_cpu = True
+    else:
+        inter = time_interleaved({"fused": fused, **legs}, args.steps, args.warmup, torch)
     torch.cuda.synchronize()
     ms = time_launches(fused, args.steps, args.warmup, torch)
     torch.cuda.synchronize()
-    if args.fused_only:
-        args.no_cpu = True
-        ms_plain = ms_unfused = ms_fused2 = float("nan")
-        ms_library = {}
-    else:
-        # the comparison legs get the same warmup, then the fused kernel is
-        # timed once more right after the unfused chain
-        ms_plain = time_launches(plain, args.steps, args.warmup, torch)
-        ms_unfused = time_launches(unfused, args.steps, args.warmup, torch)
-        ms_fused2 = time_launches(fused, args.steps, 0, torch)
-        ms_library = {k: time_launches(f, args.steps, args.warmup, torch) for k, f in library.items()}
 
     flops = 2.0 * w.M * w.N * (w.K + K2)
     tflops = flops / (ms * 1e-3) / 1e12
@@ -344,6 +509,28 @@ def main():
     traffic = stored_traffic(w.name)
     metric = METRIC if w.name == HEADLINE else (
         f"fused {idiom} TFLOP/s (2MN(K+K2)/t) fp16 on 1 MI355X; % of MFMA peak")
+    extra = None
+    if inter:
+        f_med = inter["fused"]["median_ms"]
+        extra = {
+            "frac_of_fp16_peak": round(tflops / PEAK_F16_TFLOPS, 4),
+            "interleaved": "per-launch event pairs, one launch of every leg per round, "
+                           f"{args.steps} rounds; speedups are ratios of medians",
+            "legs": inter,
+            "plain_leg": plain_leg,
+            "plain_gemm_tflops": round(2.0 * w.M * w.N * w.K / (inter["plain"]["median_ms"] * 1e-3) / 1e12, 2),
+            "unfused_chain": chain,
+            "fused_vs_unfused_speedup": round(inter["unfused_chain"]["median_ms"] / f_med, 3),
+            **({"unfused_chain2": chain2,
+                "fused_vs_unfused2_speedup": round(inter["unfused_chain2"]["median_ms"] / f_med, 3)}
+               if chain2 else {}),
+            "fused_algorithmic_GBps": round(algo_bytes / (ms * 1e-3) / 1e9, 1),
+            **({"library_legs": "torch: hipBLASLt GEMM (matmul / addmm with the bias), torch "
+                                "bias add and ReLU; context, same inputs",
+                "fused_vs_library_chain_speedup": round(inter["library_chain"]["median_ms"] / f_med, 3),
+                "fused_vs_library_gemm": round(inter["library_gemm"]["median_ms"] / f_med, 3)}
+               if "library_chain" in inter else {}),
+        }
     line = {
         "metric": metric,
         "value": round(tflops, 2),
@@ -367,22 +554,7 @@ def main():
                      "unit": "TFLOP/s", "frac": round(tflops / PEAK_F16_TFLOPS, 4),
                      "traffic": traffic},
         "cpu_baseline": cpu,
-        "extra": None if args.fused_only else {
-            "frac_of_fp16_peak": round(tflops / PEAK_F16_TFLOPS, 4),
-            "fused_ms_second_pass": round(ms_fused2, 5),
-            "plain_leg": plain_leg,
-            "plain_gemm_ms": round(ms_plain, 5),
-            "plain_gemm_tflops": round(2.0 * w.M * w.N * w.K / (ms_plain * 1e-3) / 1e12, 2),
-            "unfused_chain": chain,
-            "unfused_chain_ms": round(ms_unfused, 5),
-            "fused_vs_unfused_speedup": round(ms_unfused / ms, 3),
-            "fused_algorithmic_GBps": round(algo_bytes / (ms * 1e-3) / 1e9, 1),
-            **({"library_legs": "torch: hipBLASLt GEMM (matmul / addmm with the bias), torch "
-                                "bias add and ReLU; context, same inputs",
-                **{f"{k}_ms": round(v, 5) for k, v in ms_library.items()},
-                "fused_vs_library_chain_speedup": round(ms_library["library_chain"] / ms, 3)}
-               if ms_library else {}),
-        },
+        "extra": extra,
     }
     if args.report:
         with open(args.report, "w") as f:

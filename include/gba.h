@@ -294,13 +294,18 @@ int gba_select_tile(gba_layout layoutA, gba_layout layoutB, int64_t M, int64_t N
  *   gba_relu_f16:     C[i*ldc+j] = max(C[i*ldc+j], 0)
  *   gba_add_f16:      C[i*ldc+j] = fp16(C[i*ldc+j] + X[i*ldx+j])  (fp32 add;
  *                     the separate add of two matmul results, Listing 5)
+ *   gba_bias_act_f16: C[i*ldc+j] = fp16(act(C[i*ldc+j] + bias[j]))  (fp32;
+ *                     the bias add and activation in one pass: the second
+ *                     kernel of a two-launch chain, GEMM then bias+act)
  * Errors: GBA_EINVAL for negative sizes, ldc < N (or ldx < N), NULL C, bias
- * or X when the work is non-empty; GBA_EUNSUPPORTED for sizes above 2^31-1
+ * or X when the work is non-empty, a bad act; GBA_EUNSUPPORTED for sizes above 2^31-1
  * or pointers not 2-byte aligned; GBA_EHIP if the launch fails.
  */
 gba_status gba_bias_add_f16(int64_t M, int64_t N, void *C, int64_t ldc, const void *bias,
                             gba_stream_t stream);
 gba_status gba_relu_f16(int64_t M, int64_t N, void *C, int64_t ldc, gba_stream_t stream);
+gba_status gba_bias_act_f16(int64_t M, int64_t N, void *C, int64_t ldc, const void *bias,
+                            gba_act act, gba_stream_t stream);
 gba_status gba_add_f16(int64_t M, int64_t N, void *C, int64_t ldc, const void *X, int64_t ldx,
                        gba_stream_t stream);
 

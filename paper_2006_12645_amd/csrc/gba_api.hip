@@ -360,6 +360,39 @@ __global__ void __launch_bounds__(256) bias_add_kernel(_Float16 *C, int64_t ldc,
     }
 }
 
+// The two-launch baseline's second kernel: bias add and activation in one
+// pass, C = fp16(act(C + bias)) in fp32.
+template <bool VEC>
+__global__ void __launch_bounds__(256) bias_act_kernel(_Float16 *C, int64_t ldc, const _Float16 *bias,
+                                                       int act, int M, int N)
+{
+    const int64_t nch = (N + 7) / 8;
+    const int64_t total = (int64_t)M * nch;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = idx / nch;
+        const int j = (int)(idx - i * nch) * 8;
+        _Float16 *row = C + i * ldc + j;
+        if (VEC && j + 8 <= N) {
+            h8 c = *reinterpret_cast<const h8 *>(row);
+            const h8 b = *reinterpret_cast<const h8 *>(bias + j);
+            float x[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[e] = (float)c[e] + (float)b[e];
+            activate(act, x);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) c[e] = (_Float16)x[e];
+            *reinterpret_cast<h8 *>(row) = c;
+        } else {
+            for (int e = 0; e < 8 && j + e < N; ++e) {
+                float x[1] = {(float)row[e] + (float)bias[j + e]};
+                activate(act, x);
+                row[e] = (_Float16)x[0];
+            }
+        }
+    }
+}
+
 template <bool VEC>
 __global__ void __launch_bounds__(256) relu_kernel(_Float16 *C, int64_t ldc, int M, int N)
 {
@@ -589,6 +622,24 @@ extern "C" gba_status gba_bias_add_f16(int64_t M, int64_t N, void *C, int64_t ld
         hipLaunchKernelGGL(bias_add_kernel<true>, grid, block, 0, s, c, ldc, b, (int)M, (int)N);
     else
         hipLaunchKernelGGL(bias_add_kernel<false>, grid, block, 0, s, c, ldc, b, (int)M, (int)N);
+    return hipGetLastError() == hipSuccess ? GBA_OK : GBA_EHIP;
+}
+
+extern "C" gba_status gba_bias_act_f16(int64_t M, int64_t N, void *C, int64_t ldc, const void *bias,
+                                       gba_act act, gba_stream_t stream)
+{
+    if (act < GBA_ACT_NONE || act > GBA_ACT_TANH) return GBA_EINVAL;
+    gba_status st = validate_pointwise(M, N, C, ldc, bias, true);
+    if (st != GBA_OK || M == 0 || N == 0) return st;
+    const bool vec = aligned(C, 16) && aligned(bias, 16) && ldc % 8 == 0;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    dim3 grid(pointwise_grid(M, N)), block(256);
+    _Float16 *c = static_cast<_Float16 *>(C);
+    const _Float16 *b = static_cast<const _Float16 *>(bias);
+    if (vec)
+        hipLaunchKernelGGL(bias_act_kernel<true>, grid, block, 0, s, c, ldc, b, (int)act, (int)M, (int)N);
+    else
+        hipLaunchKernelGGL(bias_act_kernel<false>, grid, block, 0, s, c, ldc, b, (int)act, (int)M, (int)N);
     return hipGetLastError() == hipSuccess ? GBA_OK : GBA_EHIP;
 }
 

@@ -51,6 +51,7 @@ SIGNATURES = {
     "gba_select_tile": (_int, [_int, _int, _i64, _i64, _i64, _int]),
     "gba_bias_add_f16": (_int, [_i64, _i64, _vp, _i64, _vp, _vp]),
     "gba_relu_f16": (_int, [_i64, _i64, _vp, _i64, _vp]),
+    "gba_bias_act_f16": (_int, [_i64, _i64, _vp, _i64, _vp, _int, _vp]),
     "gba_add_f16": (_int, [_i64, _i64, _vp, _i64, _vp, _i64, _vp]),
     "gba_fused_desc_init": (None, [ctypes.POINTER(FusedDesc)]),
     "gba_fused_gemm": (_int, [ctypes.POINTER(FusedDesc), _vp]),
@@ -331,6 +332,16 @@ def bias_add_(C, bias, stream=None):
     return C
 
 
+def bias_act_(C, bias, act="relu", stream=None):
+    """In place: C = fp16(act(C + bias[None, :])) in one pass (the second
+    kernel of the two-launch baseline)."""
+    M, N = C.shape
+    ldc = _row_major_ld(C, "C")
+    _check(lib().gba_bias_act_f16(M, N, C.data_ptr(), ldc, bias.data_ptr(), ACTS[act],
+                                  _stream_handle(stream, C.device)), "gba_bias_act_f16")
+    return C
+
+
 def relu_(C, stream=None):
     """In place: C = max(C, 0) (unfused baseline piece)."""
     M, N = C.shape
@@ -355,6 +366,14 @@ def unfused_gemm_bias_relu(A, B, bias, out=None, tile=None, stream=None):
     out = gemm_bias_act(A, B, None, act="none", out=out, tile=tile, stream=stream)
     bias_add_(out, bias, stream)
     relu_(out, stream)
+    return out
+
+
+def unfused_gemm_bias_relu_2(A, B, bias, out=None, tile=None, stream=None):
+    """The two-launch baseline chain: GEMM (no epilogue), then bias add and
+    ReLU in one pointwise pass."""
+    out = gemm_bias_act(A, B, None, act="none", out=out, tile=tile, stream=stream)
+    bias_act_(out, bias, "relu", stream)
     return out
 
 

@@ -88,6 +88,11 @@ def test_pointwise_validation():
     assert L.gba_relu_f16(4, 4, None, 4, None) == gba.GBA_EINVAL
     assert L.gba_relu_f16(2**31, 4, FAKE, 4, None) == gba.GBA_EUNSUPPORTED
     assert L.gba_relu_f16(4, 0, None, 0, None) == gba.GBA_OK
+    assert L.gba_bias_act_f16(-1, 4, FAKE, 4, FAKE, 1, None) == gba.GBA_EINVAL
+    assert L.gba_bias_act_f16(4, 4, FAKE, 4, None, 1, None) == gba.GBA_EINVAL
+    assert L.gba_bias_act_f16(4, 4, FAKE, 4, FAKE, 9, None) == gba.GBA_EINVAL
+    assert L.gba_bias_act_f16(4, 4, FAKE + 1, 4, FAKE, 1, None) == gba.GBA_EUNSUPPORTED
+    assert L.gba_bias_act_f16(0, 4, None, 4, None, 1, None) == gba.GBA_OK
 
 
 def test_tile_table():

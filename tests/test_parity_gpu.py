@@ -387,6 +387,39 @@ def test_graph_capture_replays():
     assert not ws[:(M // 64) * (N // 64) * 4].any().item()  # the split's counters are back at 0
 
 
+def test_cube4096_two_launch_chain_full(cube4096):
+    """The two-launch baseline (GEMM, then bias add and ReLU in one pass),
+    every output against the oracle."""
+    A, B, bias, ref, _ = cube4096
+    announce("cube4096 two-launch chain RC, every output")
+    out = gba.unfused_gemm_bias_relu_2(U.device_operand(A, D.ROW), U.device_operand(B, D.COL),
+                                       torch.from_numpy(bias).cuda())
+    torch.cuda.synchronize()
+    U.assert_close(out.cpu().numpy(), ref, what="two-launch chain")
+
+
+@pytest.mark.parametrize("act", ["none", "relu", "sigmoid", "tanh"])
+def test_bias_act_piece(act):
+    """gba_bias_act_f16 against the oracle's activations: the input C stands
+    for a matmul result, so the oracle evaluates act(I.C + bias) with an
+    identity left operand (exact), and the kernel's one fp16 rounding of the
+    fp32 result must be within the fp32-accumulation bound; the aligned and
+    the scalar (odd leading dimension) paths."""
+    M, N = 64, 1031
+    announce("bias_act", act)
+    C0 = D.uniform_f16(92, (M, N), -4, 4)
+    bias = D.uniform_f16(93, (N,))
+    eye = np.eye(M, dtype=np.float16)
+    ref = O.fused(D.store(eye, D.ROW), D.ROW, D.store(C0, D.ROW), D.ROW, M, N, M, bias=bias,
+                  act={"none": O.ACT_NONE, "relu": O.ACT_RELU, "sigmoid": O.ACT_SIGMOID,
+                       "tanh": O.ACT_TANH}[act])
+    for pad in (0, 1):
+        C = U.device_operand(C0, D.ROW, pad=pad)
+        gba.bias_act_(C, torch.from_numpy(bias).cuda(), act)
+        torch.cuda.synchronize()
+        U.assert_close(C.cpu().numpy(), ref, what=f"bias_act {act} pad {pad}")
+
+
 def test_unfused_pieces():
     M, N = 333, 1031
     announce("pointwise")
