@@ -166,6 +166,7 @@ struct DmaCopy {
     int voff[NV];  // lane byte offset from the instruction's first row
     int kq[NV];    // reduction index of the lane's chunk
     int w;         // wave index (uniform)
+    int lb;        // 16 * lane: the lane's byte offset inside an instruction's KB
     int64_t ldb2;
 
     __device__ __forceinline__ void init(int64_t ld, int tid)
@@ -173,6 +174,7 @@ struct DmaCopy {
         ldb2 = ld * 2;
         w = __builtin_amdgcn_readfirstlane(tid >> 6);
         const int l = tid & 63;
+        lb = 16 * l;
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
             const int row = 8 * (NW * v + w) + (l >> 3);
@@ -193,6 +195,26 @@ struct DmaCopy {
             buffer_load16_lds(rs, stage + row0 * 128, kq[v] < kleft ? voff[v] : OOB_OFFSET,
                               (int)(row0 * ldb2));
         }
+    }
+
+    // The same copy staged through registers, for a transform between the
+    // global load and the LDS write (the prologue's ReLU): load() fetches
+    // the lane's chunks, store() writes them where dma() would have put them.
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, int kleft, i4 (&r)[NI]) const
+    {
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int v = i % NV;
+            const int row0 = 8 * (NW * i + w);
+            r[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, kq[v] < kleft ? voff[v] : OOB_OFFSET,
+                                                         (int)(row0 * ldb2), 0);
+        }
+    }
+    __device__ __forceinline__ void store(char *stage, const i4 (&r)[NI]) const
+    {
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+            *reinterpret_cast<i4 *>(stage + 8 * (NW * i + w) * 128 + lb) = r[i];
     }
 };
 
@@ -235,6 +257,7 @@ struct DmaCopyT {
     int voff[NI];  // lane byte offset from the instruction's first row
     int krow[NI];  // reduction row (inside the step) of the lane's chunk
     int w;         // wave index (uniform)
+    int lb;        // 16 * lane: the lane's byte offset inside an instruction's KB
     int64_t ldb2;
 
     __device__ __forceinline__ void init(int64_t ld, int tid)
@@ -242,6 +265,7 @@ struct DmaCopyT {
         ldb2 = ld * 2;
         w = __builtin_amdgcn_readfirstlane(tid >> 6);
         const int l = tid & 63, rl = l / CPR, p = l % CPR;
+        lb = 16 * l;
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
             const int r = (NW * i + w) * RPI + rl;
@@ -260,6 +284,22 @@ struct DmaCopyT {
             buffer_load16_lds(rs, stage + g * 1024, krow[i] < kleft ? voff[i] : OOB_OFFSET,
                               (int)(g * RPI * ldb2));
         }
+    }
+
+    // Register-staged form (as in DmaCopy).
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, int kleft, i4 (&r)[NI]) const
+    {
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int g = NW * i + w;
+            r[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, krow[i] < kleft ? voff[i] : OOB_OFFSET,
+                                                         (int)(g * RPI * ldb2), 0);
+        }
+    }
+    __device__ __forceinline__ void store(char *stage, const i4 (&r)[NI]) const
+    {
+#pragma unroll
+        for (int i = 0; i < NI; ++i) *reinterpret_cast<i4 *>(stage + (NW * i + w) * 1024 + lb) = r[i];
     }
 };
 

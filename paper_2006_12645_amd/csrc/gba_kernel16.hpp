@@ -159,10 +159,6 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
     };
     // The slice's MFMAs: A blocks q*TMH .. q*TMH+TMH-1 of half `bbuf`.
     auto mfmas = [&](int abuf, int bbuf, int q) {
-        if constexpr (PRO) {
-#pragma unroll
-            for (int s = 0; s < TMH; ++s) fa[abuf][s] = relu_h8(fa[abuf][s]);
-        }
 #pragma unroll
         for (int t = 0; t < TN; ++t)
 #pragma unroll
@@ -206,6 +202,24 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
     // the 128x64 one (three) no faster, which do not use it.
     constexpr bool PRIO = NS * STAGE <= 80 * 1024 && NS * STAGE > 160 * 1024 / 3;
     char *const mine = lds + grp * SUB;
+
+    // Prologue ReLU (Pointwise Operations in Prologue subsection), applied
+    // where the paper applies it: the left operand's tile goes from global
+    // memory into registers, through one packed max per dword, and into LDS,
+    // so each element is rectified once (not once per wave that reads it).
+    // The registers carry the next step's left tile across the step
+    // boundary: loaded with the other copies after a step's barrier, written
+    // to LDS before the next barrier.
+    static_assert(!PRO || NS == 2, "the register-staged prologue assumes two LDS stages");
+    i4 ra[PRO ? CopyA::NLOAD : 1];
+    auto relu_store_a = [&](char *stage) {
+        if constexpr (PRO) {
+#pragma unroll
+            for (int i = 0; i < CopyA::NLOAD; ++i)
+                ra[i] = __builtin_bit_cast(i4, relu_h8(__builtin_bit_cast(h8, ra[i])));
+            ca.store(stage, ra);
+        }
+    };
 
     // The row bias of this lane's output columns (4G consecutive per group
     // of G blocks), loaded before the reduction.
@@ -261,18 +275,26 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
         }
         const int nk = s_hi - s_lo;
 
+        // Copies of step s: B straight into `stage`; A too, or (prologue)
+        // into the registers ra.
         auto copy_step = [&](int s, char *stage) {
             const int k0 = __builtin_amdgcn_readfirstlane((((s < nk ? s : nk - 1) + s_lo) * SK + grp) * BK);
             const int kleft = s < nk ? Kseg - k0 : 0;
-            const auto ra = rsrc_a(k0);
-            const auto rb = rsrc_b(k0);
-            ca.dma(ra, stage, kleft);
-            cb.dma(rb, stage + BM * ROWB, kleft);
+            const auto rsa = rsrc_a(k0);
+            const auto rsb = rsrc_b(k0);
+            if constexpr (PRO) ca.load(rsa, kleft, ra);
+            else ca.dma(rsa, stage, kleft);
+            cb.dma(rsb, stage + BM * ROWB, kleft);
         };
 
         if (nk > 0) {
 #pragma unroll
-            for (int s = 0; s < NS; ++s) copy_step(s, mine + s * STAGE);
+            for (int s = 0; s < NS; ++s) {
+                copy_step(s, mine + s * STAGE);
+                // the prologue writes step 0's left tile now; step 1's stays
+                // in registers until the first step's barrier
+                if (PRO && s == 0) relu_store_a(mine);
+            }
             __builtin_amdgcn_sched_barrier(0);
             wait_vm_lgkm0<(NS - 1) * NL>();
             __builtin_amdgcn_s_barrier();
@@ -298,10 +320,16 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
             mfmas(1, 0, 1);
             round16();
             sched_slice<NM, NRB, 0, 0, false>();
-            // slice 2: half 1, first A blocks
+            // slice 2: half 1, first A blocks (prologue: plus step kt+1's
+            // rectified left tile into its stage, whose loads were issued
+            // three slices ago; kept inside this slice so that the wait for
+            // them is not hoisted to the top of the step)
+            if constexpr (PRO) __builtin_amdgcn_sched_barrier(0);
             read_a(1, cur, 1, 1);
+            relu_store_a(nxt);
             mfmas(0, 1, 0);
-            sched_slice<NM, NRA, 0, 0, false>();
+            if constexpr (PRO) sched_slice<NM, NRA, 0x200, CopyA::NLOAD, false>();
+            else sched_slice<NM, NRA, 0, 0, false>();
             if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
             // Step kt+1 complete in LDS for every wave; every read of `cur` done.
             if constexpr (VM_AT_BARRIER == 0) {
