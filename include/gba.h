@@ -179,11 +179,12 @@ void gba_fused_desc_init(gba_fused_desc *desc);
  * summation order changes, not the tolerance; GBA_ACC_F16 never splits.
  *
  * Workspace contract (gba_fused_gemm): at least this many bytes, 256-byte
- * aligned, on the device the call runs on.  It starts with one 32-bit
- * counter per output tile that must be zero when the call is enqueued and
- * is zero again when the call completes, so a workspace zero-filled once
- * serves any number of calls in stream order; calls that may run at the
- * same time need separate workspaces.  With a NULL or smaller workspace the
+ * aligned, on the device the call runs on, and all zero when the call is
+ * enqueued.  A call that splits uses it for one 32-bit counter per output
+ * tile followed by the fp32 partial tiles, and leaves every byte it used
+ * at zero again when it completes, so a workspace zero-filled once serves
+ * any number of calls in stream order, whatever their shapes and tiles;
+ * calls that may run at the same time need separate workspaces.  With a NULL or smaller workspace the
  * call runs unsplit.  split_k >= 2 asks for that many splits (fewer when
  * the reduction has fewer 64-deep steps); 0 lets the library decide.
  *

@@ -96,23 +96,44 @@ int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum);
 // fp16 accumulation the 8-wave tiles are 25-40% faster than the 4-wave
 // ones from 128x128 down and about 10% faster than 64x64 or 32x64 on the
 // small-M inference shapes (measured in the RC layout), so they come first.
+// Flops per byte of compulsory traffic (2MNK over 2(MK + KN + MN)) at the
+// ridge point of the part (2500 TFLOP/s over 8 TB/s): below it a problem
+// is bound by HBM when its operands come from there, and the four-stage
+// tiles (21-23: copies three steps ahead of the MFMAs) beat the two-stage
+// ones.
+constexpr double RIDGE_AI = 315.0;
+
 int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb)
 {
     auto tiles = [&](int t) -> int64_t {
         return tile_fits(t, M, N) ? ceil_div(M, TILES[t].bm) * ceil_div(N, TILES[t].bn) : 0;
     };
+    const double ai = (double)M * N * K / ((double)M * K + (double)K * N + (double)M * N + 1.0);
     if (tiles(1) >= 136) return 1;
     if (tiles(1) >= 112 && tiles(4) > 512) return 1;  // 128x128 would need a second round
     if (accum == GBA_ACC_F16) {
-        // fp16 accumulation: the 8-wave tiles on 16x16x32 MFMAs (their two
-        // waves per SIMD overlap one wave's rounding with the other's
-        // MFMAs), 128x128 from 128 workgroups, else 128x64 or 64x128
+        // fp16 accumulation cannot split the reduction over k-groups (one
+        // running sum).  Memory-bound problems take the four-stage tiles
+        // (measured on M = 32 / 128 / 256 x 4096 x 1024 and 1000^3 with
+        // operands from HBM: 13-19 us on the two-stage tiles against 11-12.5,
+        // about 10% slower when the operands are cache-resident); otherwise
+        // the 8-wave tiles on 16x16x32 MFMAs (their two waves per SIMD
+        // overlap one wave's rounding with the other's MFMAs), 128x128 from
+        // 128 workgroups, else 128x64 or 64x128.
         if (tiles(18) >= 128) return 18;
+        if (ai < RIDGE_AI) {
+            if (tiles(22) >= 128) return 22;
+            if (tile_fits(21, M, N)) return 21;
+            if (tile_fits(23, M, N)) return 23;
+        }
         if (tile_fits(19, M, N) && lb == GBA_COL_MAJOR) return 19;
         if (tile_fits(20, M, N) && la == GBA_ROW_MAJOR) return 20;
     }
     const int t = select_tile_rest(M, N, K, accum);
     const bool cr = la == GBA_COL_MAJOR && lb == GBA_ROW_MAJOR;
+    // memory-bound: the four-stage 64x64 tile (M = 256 x 4096 x 1024 from
+    // HBM: 8.4 against 13.7 us; about 4% slower with cache-resident operands)
+    if (t == 6 && ai < RIDGE_AI) return 22;
     return t == 4 && (accum == GBA_ACC_F16 || !cr) ? 18 : t;
 }
 

@@ -691,6 +691,20 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast(GemmArgs
                         }
                     }
             }
+            // The partials go back to zero like the counter: a later call
+            // with more output tiles keeps counters where this call kept
+            // partials, and the workspace contract is that every byte a
+            // call uses is zero when it completes.
+            for (int j = 0; j < p.splits; ++j) {
+#pragma unroll
+                for (int t = 0; t < TN; ++t)
+#pragma unroll
+                    for (int s = 0; s < TM; ++s) {
+                        f4 *dst = reinterpret_cast<f4 *>(part + (size_t)j * (BM * BN) + ((t * TM + s) * NT + tid) * 16);
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) dst[q] = f4{0.f, 0.f, 0.f, 0.f};
+                    }
+            }
             if (tid == 0)
                 __hip_atomic_store(p.counters + tile_id, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }

@@ -388,6 +388,15 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
                         acc[t][s] += *reinterpret_cast<const f4 *>(part + (size_t)j * (BM * BN) +
                                                                    ((t * TM + s) * NT + tid) * 4);
             }
+            // partials back to zero (see the 32x32 kernel)
+            for (int j = 0; j < p.splits; ++j) {
+#pragma unroll
+                for (int t = 0; t < TN; ++t)
+#pragma unroll
+                    for (int s = 0; s < TM; ++s)
+                        *reinterpret_cast<f4 *>(part + (size_t)j * (BM * BN) + ((t * TM + s) * NT + tid) * 4) =
+                            f4{0.f, 0.f, 0.f, 0.f};
+            }
             if (tid == 0)
                 __hip_atomic_store(p.counters + tile_id, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }

@@ -47,9 +47,12 @@ struct TileCfg {
     X(17, 128, 256, 4, 2, 1, 2)  \
     X(18, 128, 128, 2, 4, 1, 2)  \
     X(19, 128, 64, 4, 2, 1, 2)   \
-    X(20, 64, 128, 2, 4, 1, 2)
+    X(20, 64, 128, 2, 4, 1, 2)   \
+    X(21, 32, 64, 1, 2, 1, 4)    \
+    X(22, 64, 64, 2, 2, 1, 4)    \
+    X(23, 32, 32, 1, 1, 1, 4)
 
-constexpr int NUM_TILES = 21;
+constexpr int NUM_TILES = 24;
 
 #define GBA_TILE_CFG(id, BM, BN, WM, WN, SK, NSTG) TileCfg{BM, BN, WM, WN, SK, NSTG},
 constexpr TileCfg TILES[NUM_TILES] = {GBA_TILE_LIST(GBA_TILE_CFG)};

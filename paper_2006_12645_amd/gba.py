@@ -191,9 +191,9 @@ def workspace_size(desc):
     return n.value
 
 
-# Zero-filled workspaces, one per (device, stream): the library leaves the
-# counters at their start zero after every call, so a workspace stays ready
-# for the next call in that stream's order.  A workspace that is replaced by
+# Zero-filled workspaces, one per (device, stream): the library leaves every
+# byte a call used at zero when the call completes, so a workspace stays
+# ready for the next call in that stream's order.  A workspace that is replaced by
 # a larger one is kept alive (in _retired), since a graph captured earlier
 # may still hold its address.
 _workspaces = {}

@@ -19,7 +19,7 @@ torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
 LAYOUTS = ["RR", "RC", "CR", "CC"]
-NUM_TILES = 21
+NUM_TILES = 24
 ACT = {"none": O.ACT_NONE, "relu": O.ACT_RELU, "sigmoid": O.ACT_SIGMOID, "tanh": O.ACT_TANH}
 
 
@@ -444,6 +444,24 @@ def test_split_workspace_reused_with_new_data():
     first.gpu("RC", tile=6, split=6, workspace=ws)
     U.assert_close(second.gpu("RC", tile=6, split=6, workspace=ws), second.oracle(), what="reuse")
     assert counters_zero(ws, 6, 256, 192)
+
+
+def test_split_workspace_shared_by_different_tile_counts():
+    """Calls with different numbers of output tiles share one workspace: a
+    call with few tiles keeps partials where a later call with more tiles
+    keeps counters, so every call must leave all the bytes it used at zero
+    (a regression: the partials used to stay behind and corrupt the next
+    call's arrival counts).  Each call against the oracle, and the whole
+    workspace back at zero after each."""
+    ws = split_workspace(8 << 20)
+    for tile, M, N, K in [(9, 248, 352, 168), (21, 248, 352, 1000), (22, 136, 200, 520),
+                          (23, 248, 352, 168), (6, 200, 136, 2000), (9, 248, 352, 168)]:
+        announce("split shared ws", tile, M, N, K)
+        pr = Problem(845 + tile, M, N, K, K2=72)
+        kw = dict(prologue=True, second="sub", act="none")
+        U.assert_close(pr.gpu("RC", **kw, tile=tile, split=2, workspace=ws), pr.oracle(**kw),
+                       what=f"tile {tile} shared workspace")
+        assert not ws.any().item(), f"tile {tile} left non-zero bytes in the workspace"
 
 
 def test_library_split_on_long_reduction():
