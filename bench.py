@@ -357,6 +357,45 @@ def sweep(args, np, torch, D, gba):
     print(json.dumps(summary), flush=True)
 
 
+def ksweep(args, np, torch, D, gba):
+    """Fixed cost and cost per reduction step of the fused kernel: at fixed
+    M x N (the two MLP shapes, 1024^2 and 4096^2, RC, fp32 accumulation,
+    the library's tile choice) the reduction length K runs over 256..8192,
+    each point graph-timed (median of interleaved replays), and a least
+    squares line time = fixed + per_step * K/64 is fitted.  One JSON line per
+    point and one per fit."""
+    for (M, N) in [(8192, 4096), (8192, 1024), (1024, 1024), (4096, 4096)]:
+        ks = [256, 512, 1024, 2048, 4096, 8192]
+        legs, tiles = {}, {}
+        keep = []
+        for K in ks:
+            A, B, bias = D.random_problem(880000 + K, M, N, K)
+            dA = torch.from_numpy(A).cuda()
+            dB = torch.from_numpy(np.ascontiguousarray(B.T)).cuda().t()
+            dbias = torch.from_numpy(bias).cuda()
+            out = torch.empty((M, N), dtype=torch.float16, device="cuda")
+            keep.append((dA, dB, dbias, out))
+            tiles[K] = gba.select_tile(M, N, K)
+            legs[str(K)] = [lambda dA=dA, dB=dB, dbias=dbias, out=out, t=tiles[K]:
+                            gba.gemm_bias_act(dA, dB, dbias, act="relu", out=out, tile=t)]
+        t = graph_legs(legs, 20, 7, torch)
+        xs = [K / 64.0 for K in ks]
+        ys = [t[str(K)] * 1e3 for K in ks]
+        for K, y in zip(ks, ys):
+            print(json.dumps({"M": M, "N": N, "K": K, "tile": tiles[K], "us": round(y, 2),
+                              "TFLOP/s": round(2.0 * M * N * K / (y * 1e-6) / 1e12, 1)}), flush=True)
+        # the fit uses the points that share the K = 4096 point's tile
+        sel = [(x, y) for K, x, y in zip(ks, xs, ys) if tiles[K] == tiles[4096]]
+        n = len(sel)
+        mx = sum(x for x, _ in sel) / n
+        my = sum(y for _, y in sel) / n
+        slope = sum((x - mx) * (y - my) for x, y in sel) / sum((x - mx) ** 2 for x, _ in sel)
+        print(json.dumps({"fit": f"{M}x{N}", "tile": tiles[4096], "points": n,
+                          "fixed_us": round(my - slope * mx, 2), "per_step_us": round(slope, 4),
+                          "step_TFLOP/s": round(2.0 * M * N * 64 / (slope * 1e-6) / 1e12, 1)}), flush=True)
+        del keep
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -375,6 +414,9 @@ def main():
                     help="instead of the headline line: one JSON line per workload "
                          "configuration (every layout and accumulation it lists) with its "
                          "roofline position and fused-vs-unfused speedups")
+    ap.add_argument("--ksweep", action="store_true",
+                    help="instead of the headline line: fixed cost and cost per reduction step "
+                         "of the fused kernel from a sweep of K at fixed M x N")
     ap.add_argument("--sweep", type=int, nargs="?", const=100, default=0, metavar="N",
                     help="instead of the headline line: the paper's protocol over N random "
                          "sizes (default 100), one line per size and a summary line")
@@ -408,6 +450,9 @@ def main():
         return
     if args.sweep:
         sweep(args, np, torch, D, gba)
+        return
+    if args.ksweep:
+        ksweep(args, np, torch, D, gba)
         return
     w = D.WORKLOADS[args.workload]
     A, B, bias = D.logical_inputs(w)
