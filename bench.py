@@ -393,6 +393,20 @@ def ksweep(args, np, torch, D, gba):
         print(json.dumps({"fit": f"{M}x{N}", "tile": tiles[4096], "points": n,
                           "fixed_us": round(my - slope * mx, 2), "per_step_us": round(slope, 4),
                           "step_TFLOP/s": round(2.0 * M * N * 64 / (slope * 1e-6) / 1e12, 1)}), flush=True)
+        if (M, N) == (4096, 4096):
+            # context: the same sweep through torch's library GEMM (hipBLASLt,
+            # no epilogue) on the same operands
+            lib = {str(K): [lambda dA=dA, dB=dB, out=out: torch.matmul(dA, dB, out=out)]
+                   for K, (dA, dB, _, out) in zip(ks, keep)}
+            tl = graph_legs(lib, 20, 7, torch)
+            ly = [tl[str(K)] * 1e3 for K in ks]
+            lmy = sum(ly) / len(ly)
+            lmx = sum(xs) / len(xs)
+            ls = sum((x - lmx) * (y - lmy) for x, y in zip(xs, ly)) / sum((x - lmx) ** 2 for x in xs)
+            print(json.dumps({"fit": f"{M}x{N} library GEMM (hipBLASLt, context)", "points": len(ks),
+                              "us": {str(K): round(y, 2) for K, y in zip(ks, ly)},
+                              "fixed_us": round(lmy - ls * lmx, 2), "per_step_us": round(ls, 4),
+                              "step_TFLOP/s": round(2.0 * M * N * 64 / (ls * 1e-6) / 1e12, 1)}), flush=True)
         del keep
 
 
