@@ -1,5 +1,6 @@
 // gba_kernel16.hpp -- the fast path on v_mfma_f32_16x16x32_f16 (the 8-wave
-// tiles, every operand layout).
+// tiles, every operand layout; and the four-stage small tiles with fp16
+// accumulation when both operand tiles are reduction-contiguous).
 //
 // Same decomposition as gemm_bias_act_fast (block tile per workgroup, warp
 // tiles per wave, 64-deep reduction steps through direct global -> LDS
@@ -141,6 +142,37 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
 #pragma unroll
         for (int s = 0; s < TM; ++s) acc[t][s] = f4{0.f, 0.f, 0.f, 0.f};
 
+    // fp16 accumulation on tiles with at most one wave per SIMD: the running
+    // sum is kept as fp16 (s16) and each MFMA computes its 32-deep group's
+    // sum from zero, which is then added to the running sum with one fp32
+    // add and one rounding to fp16 (v_fma_mix: the fp16 operand is widened
+    // inside the instruction).  The MFMAs then no longer wait for the
+    // previous group's rounding -- only the adds form a chain -- which is
+    // what bounds the small memory-bound tiles; with two waves per SIMD the
+    // other wave already hides that chain, and the extra hazard waits of
+    // this form cost more than it saves.  Same result class as rounding the
+    // fp32 accumulator in place: the fp32 sum of S and the group is rounded
+    // once to fp16 (here the group's own sum is rounded to fp32 first).
+    constexpr bool FOLD = ACC16 && WM * WN < 8;
+    h4 s16[FOLD ? TN : 1][FOLD ? TM : 1];
+    float one = 1.f;
+    if constexpr (FOLD) {
+        // an opaque 1.0 keeps fma(s, 1, g) an fma, which selects v_fma_mix
+        // (with a literal 1.0 it is folded to a widening and an add)
+        asm("v_mov_b32 %0, 1.0" : "=v"(one));
+#pragma unroll
+        for (int t = 0; t < TN; ++t)
+#pragma unroll
+            for (int s = 0; s < TM; ++s) s16[t][s] = h4{0, 0, 0, 0};
+    }
+    auto fold = [&](h4 sv, f4 g) {
+        const h2v lo = {(_Float16)__builtin_fmaf((float)sv[0], one, g[0]),
+                        (_Float16)__builtin_fmaf((float)sv[1], one, g[1])};
+        const h2v hi = {(_Float16)__builtin_fmaf((float)sv[2], one, g[2]),
+                        (_Float16)__builtin_fmaf((float)sv[3], one, g[3])};
+        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3);
+    };
+
     // A fragments of two slices, B fragments of two halves.
     h8 fa[2][TMH], fb[2][TN];
     auto read_a = [&](int buf, const char *stage, int h, int q) {
@@ -162,14 +194,21 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
 #pragma unroll
         for (int t = 0; t < TN; ++t)
 #pragma unroll
-            for (int s = 0; s < TMH; ++s)
-                acc[t][q * TMH + s] =
-                    __builtin_amdgcn_mfma_f32_16x16x32_f16(fb[bbuf][t], fa[abuf][s], acc[t][q * TMH + s], 0, 0, 0);
+            for (int s = 0; s < TMH; ++s) {
+                if constexpr (FOLD) {
+                    const f4 g = __builtin_amdgcn_mfma_f32_16x16x32_f16(fb[bbuf][t], fa[abuf][s],
+                                                                        f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                    s16[t][q * TMH + s] = fold(s16[t][q * TMH + s], g);
+                } else {
+                    acc[t][q * TMH + s] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fb[bbuf][t], fa[abuf][s],
+                                                                                 acc[t][q * TMH + s], 0, 0, 0);
+                }
+            }
     };
     auto round16 = [&]() {
         // fp16 accumulation: the running sum is rounded to fp16 at the end of
         // every aligned 32-deep group of k (after both slices of a half)
-        if constexpr (ACC16) {
+        if constexpr (ACC16 && !FOLD) {
 #pragma unroll
             for (int t = 0; t < TN; ++t)
 #pragma unroll
@@ -186,7 +225,10 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
 #pragma unroll
         for (int t = 0; t < TN; ++t)
 #pragma unroll
-            for (int s = 0; s < TM; ++s) acc[t][s] = -acc[t][s];
+            for (int s = 0; s < TM; ++s) {
+                if constexpr (FOLD) s16[t][s] = -s16[t][s];
+                else acc[t][s] = -acc[t][s];
+            }
     };
 
     constexpr int NM = TN * TMH;              // MFMAs per slice
@@ -353,6 +395,14 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
 
         __builtin_amdgcn_s_waitcnt(0);
         if (seg == 1 && p.sub) negate_acc();
+    }
+    if constexpr (FOLD) {
+#pragma unroll
+        for (int t = 0; t < TN; ++t)
+#pragma unroll
+            for (int s = 0; s < TM; ++s)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc[t][s][e] = (float)s16[t][s][e];
     }
 
     if constexpr (SPLIT) {

@@ -212,7 +212,31 @@ def test_fp16_accumulation_matches_its_emulation(tile, layout):
     assert close.mean() >= 0.99, close.mean()
 
 
-@pytest.mark.parametrize("tile", [None, 1, 4, 6, 9, 18, 19, 20, "general"])
+@pytest.mark.parametrize("tile", [21, 22, 23])
+@pytest.mark.parametrize("second", [None, "add", "sub"])
+def test_fp16_accumulation_small_tiles_match_emulation(tile, second):
+    """The four-stage small tiles keep the fp16 running sum as fp16 and add
+    each 32-deep group's own fp32 sum to it (one rounding per group), in the
+    layout where both operand tiles are reduction-contiguous and without a
+    prologue: held to the oracle's emulation of the reading as the other
+    tiles are, and bit-exact on integer data."""
+    announce("f16acc small tile", tile, second)
+    kw = dict(act="none") if second is None else dict(second=second, act="none")
+    K2 = None if second is None else 200
+    pr = Problem(870 + tile, 264, 328, 1000, K2=K2, bias="row")
+    got = pr.gpu("RC", accum="f16", tile=tile, **kw).astype(np.float64)
+    emu = pr.oracle(acc16=True, **kw)
+    err = np.abs(got - emu)
+    assert (err <= 2 * ulp16(np.maximum(np.abs(emu), 64.0))).all(), err.max()
+    close = err <= 0.5 * ulp16(emu) + 1e-12
+    assert close.mean() >= 0.99, close.mean()
+    pri = Problem(880 + tile, 264, 328, 392, K2=None if second is None else 136, dist="int", full_bias=True)
+    kwi = dict(act="relu") if second is None else dict(second=second, act="relu")
+    got = pri.gpu("RC", accum="f16", tile=tile, **kwi)
+    assert np.array_equal(got.astype(np.float64), pri.oracle(**kwi)), "integer data not exact"
+
+
+@pytest.mark.parametrize("tile", [None, 1, 4, 6, 9, 18, 19, 20, 21, 22, 23, "general"])
 @pytest.mark.parametrize("layout", LAYOUTS)
 def test_fp16_accumulation_sum_of_products_golden(tile, layout):
     """The hand-derived binary16 results of the single running sum through
