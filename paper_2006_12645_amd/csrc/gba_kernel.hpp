@@ -143,6 +143,26 @@ __device__ __forceinline__ void sched_slice()
     }
 }
 
+// As sched_slice, with two classes of instructions after the reads: NA of
+// class MA spread over the first half of the slice's MFMAs, then NB of
+// class MB over the second half (the prologue's LDS writes of the staged
+// left tile, then the loads that refill its registers).
+template <int NM, int NR, int MA, int NA, int MB, int NB, int I = 0>
+__device__ __forceinline__ void sched_slice2()
+{
+    constexpr int H = NM / 2;
+    if constexpr (I == 0 && NR > 0) __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
+    if constexpr (I < NM) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        constexpr int J = I < H ? I : I - H;
+        constexpr int CNT = I < H ? NA : NB;
+        constexpr int MASK = I < H ? MA : MB;
+        constexpr int c = (CNT * (J + 1)) / H - (CNT * J) / H;
+        if constexpr (CNT > 0 && c > 0) __builtin_amdgcn_sched_group_barrier(MASK, c, 0);
+        sched_slice2<NM, NR, MA, NA, MB, NB, I + 1>();
+    }
+}
+
 // Direct global -> LDS copy of a reduction-contiguous operand tile with the
 // gfx950 buffer_load_dwordx4 ... lds form: each instruction moves 64 chunks
 // of 16 bytes into 1 KB of LDS in lane order (8 rows of 128 bytes), so lane

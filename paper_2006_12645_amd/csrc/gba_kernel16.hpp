@@ -235,7 +235,10 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
     // fragment reads (DS instructions) of slices 0, 2 and of slices 1, 3
     constexpr int NRA = TMH * (TA ? 2 : 1), NRB = NRA + TN * (TB ? 2 : 1);
     constexpr int NL = CopyA::NLOAD + CopyB::NLOAD;
-    constexpr int VM_AT_BARRIER = (NS - 2) * NL;
+    // Loads still allowed in flight at a step's barrier: the copies of the
+    // steps after the next one, and (prologue) the left tile of step kt+2,
+    // whose register loads are issued just before the barrier.
+    constexpr int VM_AT_BARRIER = (NS - 2) * NL + (PRO ? CopyA::NLOAD : 0);
     // Tiles that put two workgroups on a compute unit (by their LDS) raise
     // their waves' priority over the first three slices of a step (the
     // MFMA-only stretch), so a workgroup there is not held back by the
@@ -250,8 +253,9 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
     // memory into registers, through one packed max per dword, and into LDS,
     // so each element is rectified once (not once per wave that reads it).
     // The registers carry the next step's left tile across the step
-    // boundary: loaded with the other copies after a step's barrier, written
-    // to LDS before the next barrier.
+    // boundary: written to LDS in the third slice of a step, then loaded
+    // with the tile of the step after next right away, so the loads have a
+    // whole step to land before they are written in turn.
     static_assert(!PRO || NS == 2, "the register-staged prologue assumes two LDS stages");
     i4 ra[PRO ? CopyA::NLOAD : 1];
     auto relu_store_a = [&](char *stage) {
@@ -318,20 +322,27 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
         const int nk = s_hi - s_lo;
 
         // Copies of step s: B straight into `stage`; A too, or (prologue)
-        // into the registers ra.
+        // into the registers ra (load_a, issued separately in the loop).
+        auto step_k0 = [&](int s) {
+            return __builtin_amdgcn_readfirstlane((((s < nk ? s : nk - 1) + s_lo) * SK + grp) * BK);
+        };
+        auto load_a = [&](int s) {
+            if constexpr (PRO) {
+                const int k0 = step_k0(s);
+                ca.load(rsrc_a(k0), s < nk ? Kseg - k0 : 0, ra);
+            }
+        };
         auto copy_step = [&](int s, char *stage) {
-            const int k0 = __builtin_amdgcn_readfirstlane((((s < nk ? s : nk - 1) + s_lo) * SK + grp) * BK);
+            const int k0 = step_k0(s);
             const int kleft = s < nk ? Kseg - k0 : 0;
-            const auto rsa = rsrc_a(k0);
-            const auto rsb = rsrc_b(k0);
-            if constexpr (PRO) ca.load(rsa, kleft, ra);
-            else ca.dma(rsa, stage, kleft);
-            cb.dma(rsb, stage + BM * ROWB, kleft);
+            if constexpr (!PRO) ca.dma(rsrc_a(k0), stage, kleft);
+            cb.dma(rsrc_b(k0), stage + BM * ROWB, kleft);
         };
 
         if (nk > 0) {
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
+                load_a(s);
                 copy_step(s, mine + s * STAGE);
                 // the prologue writes step 0's left tile now; step 1's stays
                 // in registers until the first step's barrier
@@ -369,8 +380,9 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
             if constexpr (PRO) __builtin_amdgcn_sched_barrier(0);
             read_a(1, cur, 1, 1);
             relu_store_a(nxt);
+            load_a(kt + NS);
             mfmas(0, 1, 0);
-            if constexpr (PRO) sched_slice<NM, NRA, 0x200, CopyA::NLOAD, false>();
+            if constexpr (PRO) sched_slice2<NM, NRA, 0x200, CopyA::NLOAD, 0x020, CopyA::NLOAD>();
             else sched_slice<NM, NRA, 0, 0, false>();
             if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
             // Step kt+1 complete in LDS for every wave; every read of `cur` done.
