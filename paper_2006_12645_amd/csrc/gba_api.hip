@@ -123,6 +123,9 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb)
         if (tiles(18) >= 128) return 18;
         if (ai < RIDGE_AI) {
             if (tiles(22) >= 128) return 22;
+            // under 128 workgroups of 32x64, the 32x32 tile's twice as many
+            // (M = 32 x 4096 x 1024: 9.36 against 10.01 us from HBM)
+            if (tile_fits(23, M, N) && tiles(21) < 128) return 23;
             if (tile_fits(21, M, N)) return 21;
             if (tile_fits(23, M, N)) return 23;
         }
