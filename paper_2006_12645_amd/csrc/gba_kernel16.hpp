@@ -100,8 +100,21 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
     const int mc = m0 + BM <= p.M ? m0 : p.M - BM;
     const int nc = n0 + BN <= p.N ? n0 : p.N - BN;
 
-    using CopyA = std::conditional_t<TA, DmaCopyT<BM, NTG, 1>, DmaCopy<BM, NTG, 1>>;
-    using CopyB = std::conditional_t<TB, DmaCopyT<BN, NTG, 1>, DmaCopy<BN, NTG, 2>>;
+    // Which waves issue the copies.  Two waves share each SIMD; the hardware
+    // issues from the older one whenever it can, so waves 0-3 run ahead and
+    // wait at the step's barrier while waves 4-7 finish alone.  A direct
+    // copy instruction holds its wave's issue for tens of cycles, so on the
+    // one-product, single-k-group tiles the leading waves issue all of a
+    // step's copies and the trailing ones only read fragments and multiply
+    // (4096^3: 2853 -> 2688 cycles per step, measured with s_memtime; the
+    // leading waves' wait at the barrier 1096 -> 442 cycles).  The 256x128
+    // and 128x256 tiles were 1.5-3% slower that way and keep all eight
+    // waves copying.
+    constexpr bool CH = !PRO && !DUAL && !SPLIT && SK == 1 && WM * WN == 8 && BM * BN != 256 * 128;
+    constexpr int NTC = CH ? NTG / 2 : NTG;   // threads that issue the copies
+    using CopyA = std::conditional_t<TA, DmaCopyT<BM, NTC, 1>, DmaCopy<BM, NTC, 1>>;
+    using CopyB = std::conditional_t<TB, DmaCopyT<BN, NTC, 1>, DmaCopy<BN, NTC, 2>>;
+    const bool copy_wave = !CH || __builtin_amdgcn_readfirstlane(wave) < WM * WN / 2;
     CopyA ca;
     CopyB cb;
 
@@ -300,8 +313,8 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
             __syncthreads();
             if (p.sub) negate_acc();
         }
-        ca.init(ldx, gtid);
-        cb.init(ldy, gtid);
+        ca.init(ldx, CH ? (gtid & (NTC - 1)) : gtid);
+        cb.init(ldy, CH ? (gtid & (NTC - 1)) : gtid);
 
         auto rsrc_a = [&](int k0) {
             if constexpr (TA) return make_rsrc(X + (int64_t)k0 * ldx + mc, MAX_RECORDS);
@@ -343,7 +356,7 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
                 load_a(s);
-                copy_step(s, mine + s * STAGE);
+                if (copy_wave) copy_step(s, mine + s * STAGE);
                 // the prologue writes step 0's left tile now; step 1's stays
                 // in registers until the first step's barrier
                 if (PRO && s == 0) relu_store_a(mine);
@@ -359,6 +372,10 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
         // One reduction step.  On entry LDS stage `cur` holds step kt, steps
         // kt+1 .. kt+NS-1 are under way into the other stages, fa[0] holds
         // the A fragments of slice 0 and fb[0] the B fragments of half 0.
+        // (two instances of the loop: with the copies, for the waves that
+        // issue them, and without)
+        auto run_loop = [&](auto with_copies) {
+        constexpr bool WC = decltype(with_copies)::value;
         for (int kt = 0; kt < nk; ++kt) {
             char *cur = mine + (kt & (NS - 1)) * STAGE;
             char *nxt = mine + ((kt + 1) & (NS - 1)) * STAGE;
@@ -401,9 +418,12 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
             read_b(0, nxt, 0);
             mfmas(1, 1, 1);
             round16();
-            copy_step(kt + NS, cur);
-            sched_slice<NM, NRB, 0x020, NL, false>();
+            if constexpr (WC) copy_step(kt + NS, cur);
+            sched_slice<NM, NRB, 0x020, WC ? NL : 0, false>();
         }
+        };
+        if (copy_wave) run_loop(std::true_type{});
+        else run_loop(std::false_type{});
 
         __builtin_amdgcn_s_waitcnt(0);
         if (seg == 1 && p.sub) negate_acc();
