@@ -273,9 +273,17 @@ struct DmaCopyT {
     static_assert(R >= 32 && R <= 512 && (R & (R - 1)) == 0, "rows of 32 to 512 elements");
     static_assert(SW == 0 || R >= 128, "the 16x16x32 permutation needs 8 or more groups per row");
     static_assert(64 % (RPI * NW) == 0, "rows must divide evenly among the waves");
+    // A wave's consecutive instructions start RS rows apart; the chunk
+    // permutation repeats every PER rows (fT16 every 16, bswT every 4), so
+    // the lane offsets take NV distinct values.
+    static constexpr int RS = RPI * NW;
+    static constexpr int PER = SW ? 16 : 4;
+    static constexpr int NV0 = RS % PER == 0 ? 1 : PER / RS;
+    static constexpr int NV = NV0 < NI ? NV0 : NI;
+    static_assert((RS & (RS - 1)) == 0, "a power-of-two row stride");
 
-    int voff[NI];  // lane byte offset from the instruction's first row
-    int krow[NI];  // reduction row (inside the step) of the lane's chunk
+    int voff[NV];  // lane byte offset from the instruction's first row
+    int krow;      // reduction row (inside the step) of the lane's chunk in instruction 0
     int w;         // wave index (uniform)
     int lb;        // 16 * lane: the lane's byte offset inside an instruction's KB
     int64_t ldb2;
@@ -286,22 +294,24 @@ struct DmaCopyT {
         w = __builtin_amdgcn_readfirstlane(tid >> 6);
         const int l = tid & 63, rl = l / CPR, p = l % CPR;
         lb = 16 * l;
+        krow = w * RPI + rl;
 #pragma unroll
-        for (int i = 0; i < NI; ++i) {
-            const int r = (NW * i + w) * RPI + rl;
+        for (int v = 0; v < NV; ++v) {
+            const int r = krow + RS * v;
             const int col = SW ? 16 * ((p >> 1) ^ fT16(r)) + 8 * (p & 1)
                                : 32 * ((p >> 2) ^ bswT<R>(r & 3)) + 8 * (p & 3);
-            voff[i] = (int)(rl * ldb2) + 2 * col;
-            krow[i] = r;
+            voff[v] = (int)(rl * ldb2) + 2 * col;
         }
     }
 
+    // Instruction i's chunk holds reduction row krow + RS i; the bound moves
+    // to the uniform side so the comparison needs no per-instruction row.
     __device__ __forceinline__ void dma(__amdgpu_buffer_rsrc_t rs, char *stage, int kleft)
     {
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
             const int g = NW * i + w;
-            buffer_load16_lds(rs, stage + g * 1024, krow[i] < kleft ? voff[i] : OOB_OFFSET,
+            buffer_load16_lds(rs, stage + g * 1024, krow < kleft - RS * i ? voff[i % NV] : OOB_OFFSET,
                               (int)(g * RPI * ldb2));
         }
     }
@@ -312,7 +322,7 @@ struct DmaCopyT {
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
             const int g = NW * i + w;
-            r[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, krow[i] < kleft ? voff[i] : OOB_OFFSET,
+            r[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, krow < kleft - RS * i ? voff[i % NV] : OOB_OFFSET,
                                                          (int)(g * RPI * ldb2), 0);
         }
     }

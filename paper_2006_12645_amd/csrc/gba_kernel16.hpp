@@ -109,8 +109,11 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
     // (4096^3: 2853 -> 2688 cycles per step, measured with s_memtime; the
     // leading waves' wait at the barrier 1096 -> 442 cycles).  The 256x128
     // and 128x256 tiles were 1.5-3% slower that way and keep all eight
-    // waves copying.
-    constexpr bool CH = !PRO && !DUAL && !SPLIT && SK == 1 && WM * WN == 8 && BM * BN != 256 * 128;
+    // waves copying.  So do the two-product kernels (the 128x128 one grows
+    // from 87 to 137 VGPRs, one workgroup per compute unit instead of two)
+    // and the 256x256 tile with fp16 accumulation (its loops spill).
+    constexpr bool CH = !PRO && !DUAL && !SPLIT && SK == 1 && WM * WN == 8 && BM * BN != 256 * 128 &&
+                        !(ACC16 && BM * BN > 128 * 128);
     constexpr int NTC = CH ? NTG / 2 : NTG;   // threads that issue the copies
     using CopyA = std::conditional_t<TA, DmaCopyT<BM, NTC, 1>, DmaCopy<BM, NTC, 1>>;
     using CopyB = std::conditional_t<TB, DmaCopyT<BN, NTC, 1>, DmaCopy<BN, NTC, 2>>;
