@@ -71,8 +71,10 @@ int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum);
 //     a smaller tile; from 112 when 128x128 tiles (two per compute unit)
 //     would not fit in one round;
 //   * else 128x128 (two workgroups per compute unit) from 260 workgroups,
-//     then 128x64 / 64x128 (the long side along the longer output side)
-//     from 400;
+//     then 128x64 / 64x128 from 400: the 8-wave 128x64 tile on 16x16x32
+//     MFMAs when B is reduction-contiguous, the 8-wave 64x128 one when only
+//     A is, else the 4-wave tile with the long side along the longer output
+//     side;
 //   * a reduction of 1024 or more (fp32 accumulation only) whose 64x64
 //     tiles fit in one round of 160 (from K = 2048: 88) to 256 workgroups
 //     takes 64x64 with two k-groups of waves (intra-workgroup split-K) --
@@ -82,17 +84,22 @@ int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum);
 //     output tiles still, 64x64 with two k-groups while that makes more
 //     than 64 workgroups, else 32x32 with four k-groups and four LDS
 //     stages;
-//   * else 64x64 from 200 workgroups, then 32x64 -- replaced, for fp32
+//   * else 64x64 from 160 workgroups (in RC, the four-stage 64x64 tile
+//     instead for K >= 1792 over at most 512 of them), then 32x64 --
+//     replaced, for fp32
 //     accumulation and K >= 768, by 32x32 with four k-groups when that
 //     makes at most 128 workgroups, else by 32x64 with four k-groups when
 //     that makes at most 256 -- then 32x32.
 // The 256x128 and 128x256 tiles (4 or 8 waves) were never clearly the
 // fastest in those sweeps and are only used when asked for.  128x128 means
 // the 8-wave tile on 16x16x32 MFMAs: with fp32 accumulation 3-6% faster
-// than the 4-wave one over the shapes the rule gives it (over two sweeps of
-// random shapes the rule is then 0.8-0.9% slower in total than the
-// per-shape best tile in the RC layout), except with column-major A and
-// row-major B, where the two were within a few percent either way.  With
+// than the 4-wave one over the shapes the rule gives it, except with
+// column-major A and row-major B, where the two were within a few percent
+// either way.  Over four sets of 51 shapes in RC (two of them held out from
+// the fitting) the rule is 0.35-0.5% slower in total than the per-shape
+// best tile (1.3-1.5% before the 8-wave 128x64 / 64x128 tiles and the
+// four-stage 64x64 one took the shapes above); over one set each, 2.1% in
+// RR, 1.0% in CC and 4.2% in CR.  With
 // fp16 accumulation the 8-wave tiles are 25-40% faster than the 4-wave
 // ones from 128x128 down and about 10% faster than 64x64 or 32x64 on the
 // small-M inference shapes (measured in the RC layout), so they come first.
@@ -145,9 +152,19 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb)
     }
     const int t = select_tile_rest(M, N, K, accum);
     const bool cr = la == GBA_COL_MAJOR && lb == GBA_ROW_MAJOR;
+    const bool rc = la == GBA_ROW_MAJOR && lb == GBA_COL_MAJOR;
     // memory-bound: the four-stage 64x64 tile (M = 256 x 4096 x 1024 from
     // HBM: 8.4 against 13.7 us; about 4% slower with cache-resident operands)
     if (t == 6 && ai < RIDGE_AI) return 22;
+    // long reductions over at most two rounds of 64x64 tiles: the four-stage
+    // tile again (RC only; its transposed copies lose in the other layouts)
+    if (t == 6 && rc && tiles(6) <= 512 && K >= 1792) return 22;
+    // 128x64 / 64x128: the 8-wave 128x64 tile on 16x16x32 MFMAs where B is
+    // reduction-contiguous, the 8-wave 64x128 one where only A is
+    if (t == 5 || t == 7) {
+        if (lb == GBA_COL_MAJOR) return 19;
+        if (la == GBA_ROW_MAJOR) return 20;
+    }
     return t == 4 && (accum == GBA_ACC_F16 || !cr) ? 18 : t;
 }
 
@@ -169,7 +186,7 @@ int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum)
             if (tile_fits(13, M, N)) return 13;
         }
     }
-    if (tiles(6) >= 200) return 6;
+    if (tiles(6) >= 160) return 6;
     if (tile_fits(8, M, N)) {
         // few 32x64 tiles over a reduction of 768 or more: the k-group
         // tiles keep more waves busy per output tile
