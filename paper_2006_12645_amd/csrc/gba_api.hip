@@ -120,32 +120,36 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb)
     if (tiles(1) >= 112 && tiles(4) > 512) return 1;  // 128x128 would need a second round
     if (accum == GBA_ACC_F16) {
         // fp16 accumulation cannot split the reduction over k-groups (one
-        // running sum).  Thin memory-bound problems (at most 256 rows or
-        // columns) take the four-stage tiles (measured on M = 32 / 128 / 256
-        // x 4096 x 1024 and 1000^3 with operands from HBM: 13-19 us on the
-        // two-stage tiles against 11-12.5); otherwise the 8-wave tiles on
-        // 16x16x32 MFMAs (their two waves per SIMD overlap one wave's
-        // rounding with the other's MFMAs): 128x128 for one round of short
-        // reductions (K <= 1024, 128-255 workgroups) and from 384 workgroups,
-        // else 64x128 or 128x64 -- with both operand tiles
-        // reduction-contiguous 64x128, 3-6% faster on most shapes measured --
-        // and for long reductions over one round of 64x64 tiles the
-        // four-stage 64x64 tile, whose fp16 running sum keeps its MFMAs
-        // independent (1024 x 1024 x 4096: 29.0 against 36.6 us).  Over 36
-        // random shapes in the RC layout this is 1.5% slower in total than
-        // the per-shape best tile, against 6.3% for the rule before it.
+        // running sum).  In RC the small tiles run with copy-only waves
+        // beside the computing ones, which keeps enough bytes in flight from
+        // HBM: the 32x32 tile while it makes at most one round of 256
+        // workgroups, else the 32x64 one, else the 64x64 one up to 640
+        // workgroups (on 72 random RC shapes and 66 thin ones, warm and with
+        // operands from HBM: 1.1% and 0.4% slower in total than the
+        // per-shape best tile, against 4.9% and 16% for the rule before;
+        // the 8-wave tiles keep two stages and pull less from HBM: 896 x
+        // 1536 x 1024, 15.6 against 11.8 us cold).  Larger problems, and
+        // thin memory-bound ones in the other layouts (the four-stage tiles
+        // there, measured on M = 32 / 128 / 256 x 4096 x 1024 and 1000^3:
+        // 13-19 us on the two-stage tiles against 11-12.5), then the 8-wave
+        // tiles on 16x16x32 MFMAs (their two waves per SIMD overlap one
+        // wave's rounding with the other's MFMAs): 128x128 for one round of
+        // short reductions (K <= 1024, 128-255 workgroups) and from 384
+        // workgroups, else 64x128 or 128x64 -- with both operand tiles
+        // reduction-contiguous 64x128.
         const bool rc = la == GBA_ROW_MAJOR && lb == GBA_COL_MAJOR;
-        if (ai < RIDGE_AI && (M <= 256 || N <= 256)) {
+        if (rc) {
+            if (tile_fits(23, M, N) && tiles(23) <= 256) return 23;
+            if (tile_fits(21, M, N) && tiles(21) <= 256) return 21;
+            if (tile_fits(22, M, N) && tiles(22) <= 640) return 22;
+        } else if (ai < RIDGE_AI && (M <= 256 || N <= 256)) {
             if (tiles(22) >= 128) return 22;
-            // under 128 workgroups of 32x64, the 32x32 tile's twice as many
-            // (M = 32 x 4096 x 1024: 9.36 against 10.01 us from HBM)
             if (tile_fits(23, M, N) && tiles(21) < 128) return 23;
             if (tile_fits(21, M, N)) return 21;
             if (tile_fits(23, M, N)) return 23;
         }
         const int64_t t18 = tiles(18);
         if (t18 >= 384 || (t18 >= 128 && t18 < 256 && K <= 1024)) return 18;
-        if (rc && K >= 4096 && tiles(22) >= 128 && tiles(22) <= 256) return 22;
         if (tile_fits(20, M, N) && la == GBA_ROW_MAJOR) return 20;
         if (tile_fits(19, M, N) && lb == GBA_COL_MAJOR) return 19;
         if (t18 >= 128) return 18;

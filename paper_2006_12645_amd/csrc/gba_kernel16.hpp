@@ -52,12 +52,27 @@ __device__ __forceinline__ int perm16(int t, int rho)
     return 16 * G * (t / G) + 4 * G * (rho >> 2) + 4 * (t % G) + (rho & 3);
 }
 
+// Waves that only issue copies, added to the workgroups of the small tiles
+// with fp16 accumulation (one or four computing waves, latency-bound: with
+// the copies on the computing waves each 64-deep step waits for their
+// issue).  Four of them: 32 x 4096 x 1024 on the 32x32 tile 9.2 -> 6.8 us,
+// 1024 x 1024 x 4096 on the 64x64 tile 28.2 -> 21.7 us (one or two gave
+// less).  Not with the prologue, whose left tile is staged through the
+// computing waves' registers.
+template <int WM, int WN, int SK, bool ACC16, bool PRO, bool SPLIT>
+constexpr int copy_only_waves()
+{
+    return (ACC16 && WM * WN < 8 && SK == 1 && !PRO && !SPLIT) ? 4 : 0;
+}
+
 template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool PRO, bool DUAL,
           bool SPLIT>
-__global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmArgs p)
+__global__ void __launch_bounds__(64 * (WM * WN * SK + copy_only_waves<WM, WN, SK, ACC16, PRO, SPLIT>()))
+gemm_bias_act_fast16(GemmArgs p)
 {
     constexpr int NTG = 64 * WM * WN;         // threads per k-group
-    constexpr int NT = NTG * SK;
+    constexpr int NT = NTG * SK;              // threads that compute
+    constexpr int NPW = copy_only_waves<WM, WN, SK, ACC16, PRO, SPLIT>();
     constexpr int BK = 64;
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int TM = WTM / 16, TN = WTN / 16;   // 16x16 blocks of the warp tile
@@ -84,7 +99,7 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int grp = wave / (WM * WN);         // k-group
+    const int grp = SK == 1 ? 0 : wave / (WM * WN);   // k-group
     const int gtid = tid - grp * NTG;         // thread index inside the k-group
     const int wm = (wave % (WM * WN)) % WM, wn = (wave % (WM * WN)) / WM;
     const int l16 = lane & 15, g4 = lane >> 4;
@@ -114,10 +129,12 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
     // and the 256x256 tile with fp16 accumulation (its loops spill).
     constexpr bool CH = !PRO && !DUAL && !SPLIT && SK == 1 && WM * WN == 8 && BM * BN != 256 * 128 &&
                         !(ACC16 && BM * BN > 128 * 128);
-    constexpr int NTC = CH ? NTG / 2 : NTG;   // threads that issue the copies
+    constexpr int NTC = NPW ? 64 * NPW : CH ? NTG / 2 : NTG;   // threads that issue the copies
     using CopyA = std::conditional_t<TA, DmaCopyT<BM, NTC, 1>, DmaCopy<BM, NTC, 1>>;
     using CopyB = std::conditional_t<TB, DmaCopyT<BN, NTC, 1>, DmaCopy<BN, NTC, 2>>;
-    const bool copy_wave = !CH || __builtin_amdgcn_readfirstlane(wave) < WM * WN / 2;
+    const int rwave = __builtin_amdgcn_readfirstlane(wave);
+    const bool copy_wave = NPW ? rwave >= WM * WN : (!CH || rwave < WM * WN / 2);
+    const int ctid = NPW ? tid - NT : CH ? (gtid & (NTC - 1)) : gtid;   // thread index among the copiers
     CopyA ca;
     CopyB cb;
 
@@ -316,8 +333,8 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
             __syncthreads();
             if (p.sub) negate_acc();
         }
-        ca.init(ldx, CH ? (gtid & (NTC - 1)) : gtid);
-        cb.init(ldy, CH ? (gtid & (NTC - 1)) : gtid);
+        ca.init(ldx, ctid);
+        cb.init(ldy, ctid);
 
         auto rsrc_a = [&](int k0) {
             if constexpr (TA) return make_rsrc(X + (int64_t)k0 * ldx + mc, MAX_RECORDS);
@@ -368,8 +385,27 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
             wait_vm_lgkm0<(NS - 1) * NL>();
             __builtin_amdgcn_s_barrier();
             __builtin_amdgcn_sched_barrier(0);
-            read_a(0, mine, 0, 0);
-            read_b(0, mine, 0);
+            if (NPW == 0 || !copy_wave) {
+                read_a(0, mine, 0, 0);
+                read_b(0, mine, 0);
+            }
+        }
+        if constexpr (NPW > 0) {
+            // Copy-only waves: the barrier of every step, as the computing
+            // waves (step kt+1 landed, step kt's stage released), then the
+            // copies of step kt+NS into that stage.
+            if (copy_wave) {
+                for (int kt = 0; kt < nk; ++kt) {
+                    char *cur = mine + (kt & (NS - 1)) * STAGE;
+                    __builtin_amdgcn_sched_barrier(0);
+                    wait_vm_lgkm0<VM_AT_BARRIER>();
+                    __builtin_amdgcn_s_barrier();
+                    __builtin_amdgcn_sched_barrier(0);
+                    copy_step(kt + NS, cur);
+                }
+                __builtin_amdgcn_s_waitcnt(0);
+                continue;
+            }
         }
 
         // One reduction step.  On entry LDS stage `cur` holds step kt, steps
@@ -431,6 +467,8 @@ __global__ void __launch_bounds__(64 * WM * WN * SK) gemm_bias_act_fast16(GemmAr
         __builtin_amdgcn_s_waitcnt(0);
         if (seg == 1 && p.sub) negate_acc();
     }
+    // the copy-only waves are done (the epilogue has no barrier)
+    if (NPW > 0 && copy_wave) return;
     if constexpr (FOLD) {
 #pragma unroll
         for (int t = 0; t < TN; ++t)

@@ -99,7 +99,9 @@ template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool
 hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
 {
     // one workgroup per output tile, times the splits of its reduction
-    dim3 grid((unsigned)(a.tiles_m * a.tiles_n * (SPLIT ? a.splits : 1))), block(64 * WM * WN * SK);
+    constexpr int NPW = use_fast16(LA, LB, BM, BN, WM, WN, SK, NSTG, ACC16, PRO)
+                            ? copy_only_waves<WM, WN, SK, ACC16, PRO, SPLIT>() : 0;
+    dim3 grid((unsigned)(a.tiles_m * a.tiles_n * (SPLIT ? a.splits : 1))), block(64 * (WM * WN * SK + NPW));
     // The 8-wave tiles (one k-group) run on 16x16x32 MFMAs, and so do the
     // four-stage small tiles with fp16 accumulation (use_fast16);
     // everything else on 32x32x16 (measured per tile: the 16x16x32 kernels

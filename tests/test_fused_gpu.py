@@ -236,6 +236,28 @@ def test_fp16_accumulation_small_tiles_match_emulation(tile, second):
     assert np.array_equal(got.astype(np.float64), pri.oracle(**kwi)), "integer data not exact"
 
 
+@pytest.mark.parametrize("tile", [21, 22, 23])
+@pytest.mark.parametrize("K,K2", [(8, None), (64, None), (136, None), (256, None), (328, None), (40, 72),
+                                  (256, 8)])
+def test_fp16_accumulation_small_tiles_step_counts(tile, K, K2):
+    """Reductions of one step, of fewer steps than the four LDS stages, of
+    exactly four and of more, in one and in two products, on the small
+    tiles with fp16 accumulation, whose copies are issued by waves that do
+    not compute: each step's barrier must pair up between the two kinds of
+    waves, and the copies past the last step must stay out of the result."""
+    announce("f16acc small tile steps", tile, K, K2)
+    kw = dict(act="none") if K2 is None else dict(second="sub", act="none")
+    pr = Problem(900 + tile + K, 96, 160, K, K2=K2, bias="row")
+    got = pr.gpu("RC", accum="f16", tile=tile, **kw).astype(np.float64)
+    emu = pr.oracle(acc16=True, **kw)
+    err = np.abs(got - emu)
+    assert (err <= 2 * ulp16(np.maximum(np.abs(emu), 64.0))).all(), err.max()
+    pri = Problem(950 + tile + K, 96, 160, K, K2=K2, dist="int", full_bias=True)
+    kwi = dict(act="relu") if K2 is None else dict(second="add", act="relu")
+    got = pri.gpu("RC", accum="f16", tile=tile, **kwi)
+    assert np.array_equal(got.astype(np.float64), pri.oracle(**kwi)), "integer data not exact"
+
+
 @pytest.mark.parametrize("tile", [None, 1, 4, 6, 9, 18, 19, 20, 21, 22, 23, "general"])
 @pytest.mark.parametrize("layout", LAYOUTS)
 def test_fp16_accumulation_sum_of_products_golden(tile, layout):
