@@ -127,7 +127,19 @@ gemm_bias_act_fast16(GemmArgs p)
     // waves copying.  So do the two-product kernels (the 128x128 one grows
     // from 87 to 137 VGPRs, one workgroup per compute unit instead of two)
     // and the 256x256 tile with fp16 accumulation (its loops spill).
-    constexpr bool CH = !PRO && !DUAL && !SPLIT && SK == 1 && WM * WN == 8 && BM * BN != 256 * 128 &&
+    // The prologue ReLU either on the A fragments as they are read (the left
+    // tile then comes in by direct copies, and the copy split below applies)
+    // or on the left tile staged through registers (where the tile is
+    // written into LDS).  On the fragments each of the WN waves that read an
+    // A block rectifies it again (one packed integer max per dword), which
+    // measured: 4096^3 RC 109.5 -> 107.1 us (the kernel without prologue
+    // 107.0), RR 117.5 -> 112.1, 8192x4096x1024 69.7 -> 67.1; the 8-wave
+    // 128x64 / 64x128 tiles 7-9% faster; slower with column-major A (its
+    // transposing fragment reads; 1.5-2%) and on the 128x128 tile (5-15%),
+    // which keep the staged tile.
+    constexpr bool PROF = PRO && LA == ROW && WM * WN == 8 && (BM * BN == 256 * 256 || BM * BN == 128 * 64);
+    constexpr bool PROS = PRO && !PROF;            // register-staged left tile
+    constexpr bool CH = !PROS && !DUAL && !SPLIT && SK == 1 && WM * WN == 8 && BM * BN != 256 * 128 &&
                         !(ACC16 && BM * BN > 128 * 128);
     constexpr int NTC = NPW ? 64 * NPW : CH ? NTG / 2 : NTG;   // threads that issue the copies
     using CopyA = std::conditional_t<TA, DmaCopyT<BM, NTC, 1>, DmaCopy<BM, NTC, 1>>;
@@ -213,6 +225,7 @@ gemm_bias_act_fast16(GemmArgs p)
         for (int s = 0; s < TMH; ++s) {
             if constexpr (TA) fa[buf][s] = read_frag_tr<BM>(stage + offa[q * TMH + s] + h * 32 * (2 * BM));
             else fa[buf][s] = *reinterpret_cast<const h8 *>(stage + offa[h] + (q * TMH + s) * 16 * ROWB);
+            if constexpr (PROF) fa[buf][s] = relu_h8(fa[buf][s]);
         }
     };
     auto read_b = [&](int buf, const char *stage, int h) {
@@ -271,7 +284,7 @@ gemm_bias_act_fast16(GemmArgs p)
     // Loads still allowed in flight at a step's barrier: the copies of the
     // steps after the next one, and (prologue) the left tile of step kt+2,
     // whose register loads are issued just before the barrier.
-    constexpr int VM_AT_BARRIER = (NS - 2) * NL + (PRO ? CopyA::NLOAD : 0);
+    constexpr int VM_AT_BARRIER = (NS - 2) * NL + (PROS ? CopyA::NLOAD : 0);
     // Tiles that put two workgroups on a compute unit (by their LDS) raise
     // their waves' priority over the first three slices of a step (the
     // MFMA-only stretch), so a workgroup there is not held back by the
@@ -281,18 +294,19 @@ gemm_bias_act_fast16(GemmArgs p)
     constexpr bool PRIO = NS * STAGE <= 80 * 1024 && NS * STAGE > 160 * 1024 / 3;
     char *const mine = lds + grp * SUB;
 
-    // Prologue ReLU (Pointwise Operations in Prologue subsection), applied
-    // where the paper applies it: the left operand's tile goes from global
-    // memory into registers, through one packed max per dword, and into LDS,
-    // so each element is rectified once (not once per wave that reads it).
+    // Prologue ReLU (Pointwise Operations in Prologue subsection), on the
+    // tiles that do not rectify their A fragments (PROF) applied where the
+    // paper applies it: the left operand's tile goes from global memory
+    // into registers, through one packed max per dword, and into LDS, so
+    // each element is rectified once (not once per wave that reads it).
     // The registers carry the next step's left tile across the step
     // boundary: written to LDS in the third slice of a step, then loaded
     // with the tile of the step after next right away, so the loads have a
     // whole step to land before they are written in turn.
-    static_assert(!PRO || NS == 2, "the register-staged prologue assumes two LDS stages");
-    i4 ra[PRO ? CopyA::NLOAD : 1];
+    static_assert(!PROS || NS == 2, "the register-staged prologue assumes two LDS stages");
+    i4 ra[PROS ? CopyA::NLOAD : 1];
     auto relu_store_a = [&](char *stage) {
-        if constexpr (PRO) {
+        if constexpr (PROS) {
 #pragma unroll
             for (int i = 0; i < CopyA::NLOAD; ++i)
                 ra[i] = __builtin_bit_cast(i4, relu_h8(__builtin_bit_cast(h8, ra[i])));
@@ -360,7 +374,7 @@ gemm_bias_act_fast16(GemmArgs p)
             return __builtin_amdgcn_readfirstlane((((s < nk ? s : nk - 1) + s_lo) * SK + grp) * BK);
         };
         auto load_a = [&](int s) {
-            if constexpr (PRO) {
+            if constexpr (PROS) {
                 const int k0 = step_k0(s);
                 ca.load(rsrc_a(k0), s < nk ? Kseg - k0 : 0, ra);
             }
@@ -368,7 +382,7 @@ gemm_bias_act_fast16(GemmArgs p)
         auto copy_step = [&](int s, char *stage) {
             const int k0 = step_k0(s);
             const int kleft = s < nk ? Kseg - k0 : 0;
-            if constexpr (!PRO) ca.dma(rsrc_a(k0), stage, kleft);
+            if constexpr (!PROS) ca.dma(rsrc_a(k0), stage, kleft);
             cb.dma(rsrc_b(k0), stage + BM * ROWB, kleft);
         };
 
@@ -379,7 +393,7 @@ gemm_bias_act_fast16(GemmArgs p)
                 if (copy_wave) copy_step(s, mine + s * STAGE);
                 // the prologue writes step 0's left tile now; step 1's stays
                 // in registers until the first step's barrier
-                if (PRO && s == 0) relu_store_a(mine);
+                if (PROS && s == 0) relu_store_a(mine);
             }
             __builtin_amdgcn_sched_barrier(0);
             wait_vm_lgkm0<(NS - 1) * NL>();
@@ -433,12 +447,12 @@ gemm_bias_act_fast16(GemmArgs p)
             // rectified left tile into its stage, whose loads were issued
             // three slices ago; kept inside this slice so that the wait for
             // them is not hoisted to the top of the step)
-            if constexpr (PRO) __builtin_amdgcn_sched_barrier(0);
+            if constexpr (PROS) __builtin_amdgcn_sched_barrier(0);
             read_a(1, cur, 1, 1);
             relu_store_a(nxt);
             load_a(kt + NS);
             mfmas(0, 1, 0);
-            if constexpr (PRO) sched_slice2<NM, NRA, 0x200, CopyA::NLOAD, 0x020, CopyA::NLOAD>();
+            if constexpr (PROS) sched_slice2<NM, NRA, 0x200, CopyA::NLOAD, 0x020, CopyA::NLOAD>();
             else sched_slice<NM, NRA, 0, 0, false>();
             if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
             // Step kt+1 complete in LDS for every wave; every read of `cur` done.

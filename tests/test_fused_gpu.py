@@ -175,6 +175,20 @@ def test_every_tile_all_features(tile):
     U.assert_close(pr.gpu("RC", **kw, tile=tile), pr.oracle(**kw), what=f"tile {tile}")
 
 
+@pytest.mark.parametrize("tile", [1, 16, 17, 18, 19, 20])
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("accum", ["f32", "f16"])
+def test_prologue_on_eight_wave_tiles(tile, layout, accum):
+    """The prologue ReLU on the 8-wave tiles, one product: on some of them
+    (row-major A) the A fragments are rectified as they are read and the
+    left tile arrives by direct copies, on the others the left tile is
+    staged through registers; both must give the oracle's result."""
+    announce("prologue 8-wave", tile, layout, accum)
+    pr = Problem(1000 + tile, 264, 328, 200, bias="row")
+    U.assert_close(pr.gpu(layout, prologue=True, accum=accum, tile=tile), pr.oracle(prologue=True, acc16=accum == "f16"),
+                   accum=accum, what=f"prologue tile {tile} {layout} {accum}")
+
+
 @pytest.mark.parametrize("tile", [1, 4, 6, 9])
 @pytest.mark.parametrize("layout", ["RC", "CR"])
 def test_fp16_accumulation_two_products(tile, layout):
