@@ -252,13 +252,14 @@ def test_fp16_accumulation_small_tiles_match_emulation(tile, second):
 
 @pytest.mark.parametrize("tile", [21, 22, 23])
 @pytest.mark.parametrize("K,K2", [(8, None), (64, None), (136, None), (256, None), (328, None), (40, 72),
-                                  (256, 8)])
+                                  (256, 8), (0, 64), (64, 0), (0, 0)])
 def test_fp16_accumulation_small_tiles_step_counts(tile, K, K2):
     """Reductions of one step, of fewer steps than the four LDS stages, of
-    exactly four and of more, in one and in two products, on the small
-    tiles with fp16 accumulation, whose copies are issued by waves that do
-    not compute: each step's barrier must pair up between the two kinds of
-    waves, and the copies past the last step must stay out of the result."""
+    exactly four and of more, and empty ones, in one and in two products, on
+    the small tiles with fp16 accumulation, whose copies are issued by waves
+    that do not compute: each step's barrier must pair up between the two
+    kinds of waves, and the copies past the last step must stay out of the
+    result."""
     announce("f16acc small tile steps", tile, K, K2)
     kw = dict(act="none") if K2 is None else dict(second="sub", act="none")
     pr = Problem(900 + tile + K, 96, 160, K, K2=K2, bias="row")
