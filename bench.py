@@ -69,6 +69,26 @@ def stored_traffic(workload):
     return float(m_b.group(1))
 
 
+def stored_clock_peak():
+    """Observed shader clock (GHz) and the clock-adjusted fp16 MFMA peak
+    (TFLOP/s: 256 CUs x 4096 flop per clock x that clock) of the headline
+    kernel from the committed rocprofv3 MFMA-utilisation summary, or None
+    when absent or taken on different kernel sources."""
+    path = os.path.join(PROFILES, f"gemm_bias_act_{HEADLINE}_mfma_util.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
+    row = re.search(r"^\| `gemm_bias_act_fast16<256, 256[^`]*` \|([^\n]*)$", text, re.M)
+    if not m_sha or not row or m_sha.group(1) != kernel_source_digest():
+        return None
+    cols = [c.strip() for c in row.group(1).split("|")]
+    try:
+        return float(cols[3]), float(cols[4])
+    except (IndexError, ValueError):
+        return None
+
+
 def time_launches(fn, steps, warmup, torch):
     """Average ms per call of fn over `steps` calls (after `warmup`), timed
     with events on the current stream, which is where the library launches."""
@@ -566,6 +586,7 @@ def main():
         cpu = cpu_baseline(w, A, B, bias, P, Q)
 
     traffic = stored_traffic(w.name)
+    clk = stored_clock_peak()
     metric = METRIC if w.name == HEADLINE else (
         f"fused {idiom} TFLOP/s (2MN(K+K2)/t) fp16 on 1 MI355X; % of MFMA peak")
     extra = None
@@ -584,6 +605,11 @@ def main():
                 "fused_vs_unfused2_speedup": round(inter["unfused_chain2"]["median_ms"] / f_med, 3)}
                if chain2 else {}),
             "fused_algorithmic_GBps": round(algo_bytes / (ms * 1e-3) / 1e9, 1),
+            **({"clock_adjusted_peak": {
+                    "sclk_GHz": clk[0], "peak_TFLOPs": clk[1], "frac": round(tflops / clk[1], 4),
+                    "source": f"profiles/gemm_bias_act_{HEADLINE}_mfma_util.md (GRBM_GUI_ACTIVE over "
+                              "the dispatch time, another run on another box)"}}
+               if clk and w.name == HEADLINE else {}),
             **({"library_legs": "torch: hipBLASLt GEMM (matmul / addmm with the bias), torch "
                                 "bias add and ReLU; context, same inputs",
                 "fused_vs_library_chain_speedup": round(inter["library_chain"]["median_ms"] / f_med, 3),
