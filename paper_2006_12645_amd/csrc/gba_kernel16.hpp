@@ -1,6 +1,6 @@
 // gba_kernel16.hpp -- the fast path on v_mfma_f32_16x16x32_f16 (the 8-wave
-// tiles, every operand layout; and the four-stage small tiles with fp16
-// accumulation when both operand tiles are reduction-contiguous).
+// tiles, every operand layout; and the four-stage small tiles when both
+// operand tiles are reduction-contiguous).
 //
 // Same decomposition as gemm_bias_act_fast (block tile per workgroup, warp
 // tiles per wave, 64-deep reduction steps through direct global -> LDS
@@ -53,16 +53,16 @@ __device__ __forceinline__ int perm16(int t, int rho)
 }
 
 // Waves that only issue copies, added to the workgroups of the small tiles
-// with fp16 accumulation (one or four computing waves, latency-bound: with
-// the copies on the computing waves each 64-deep step waits for their
-// issue).  Four of them: 32 x 4096 x 1024 on the 32x32 tile 9.2 -> 6.8 us,
+// (one, two or four computing waves, latency-bound: with the copies on the
+// computing waves each 64-deep step waits for their issue).  Four of them,
+// with fp16 accumulation: 32 x 4096 x 1024 on the 32x32 tile 9.2 -> 6.8 us,
 // 1024 x 1024 x 4096 on the 64x64 tile 28.2 -> 21.7 us (one or two gave
 // less).  Not with the prologue, whose left tile is staged through the
 // computing waves' registers.
 template <int WM, int WN, int SK, bool ACC16, bool PRO, bool SPLIT>
 constexpr int copy_only_waves()
 {
-    return (ACC16 && WM * WN < 8 && SK == 1 && !PRO && !SPLIT) ? 4 : 0;
+    return (WM * WN < 8 && SK == 1 && !PRO && !SPLIT) ? 4 : 0;
 }
 
 template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool PRO, bool DUAL,

@@ -81,17 +81,21 @@ struct LayoutTable {
 // Which tiles run the 16x16x32 kernel (gemm_bias_act_fast16): the ones
 // with eight waves of one k-group, in every layout where an M- or
 // N-contiguous operand tile has 128 or more elements per row (its
-// conflict-free group permutation needs eight 16-element groups); and, with
-// fp16 accumulation and no prologue, the four-stage small tiles (21-23) in
-// the layouts where both operand tiles are reduction-contiguous, where the
-// 16x16x32 kernel's fp16 running sum breaks the chain of dependent MFMAs
-// that bounds these latency-bound tiles (M = 32 / 128 / 256 x 4096 x 1024
-// from HBM: 10.7 / 11.1 / 11.4 against 9.7-9.8 us, graph-timed).
-constexpr bool use_fast16(int la, int lb, int bm, int bn, int wm, int wn, int sk, int nstg, bool acc16, bool pro)
+// conflict-free group permutation needs eight 16-element groups); and,
+// without prologue and unless the reduction is split across workgroups,
+// the four-stage small tiles (21-23) in the layout where both operand tiles
+// are reduction-contiguous, where the 16x16x32 kernel adds waves that only
+// issue copies (with fp16 accumulation its fp16 running sum also breaks the
+// chain of dependent MFMAs).  With fp32 accumulation that is 6-10% faster
+// than these tiles on 32x32x16 without copy-only waves, and than the
+// k-group tiles on 1024^3 (6.66 against 7.33 us) and 1000^3 (6.99 against
+// 7.75).
+constexpr bool use_fast16(int la, int lb, int bm, int bn, int wm, int wn, int sk, int nstg, bool acc16, bool pro,
+                          bool split = false)
 {
     const bool layouts = (bm >= 128 || la == ROW) && (bn >= 128 || lb == COL);
     if (wm * wn == 8) return layouts;
-    return acc16 && !pro && sk == 1 && nstg == 4 && layouts;
+    return (acc16 || !split) && !pro && sk == 1 && nstg == 4 && layouts;
 }
 
 template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool PRO, bool DUAL,
@@ -99,16 +103,16 @@ template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool
 hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
 {
     // one workgroup per output tile, times the splits of its reduction
-    constexpr int NPW = use_fast16(LA, LB, BM, BN, WM, WN, SK, NSTG, ACC16, PRO)
+    constexpr int NPW = use_fast16(LA, LB, BM, BN, WM, WN, SK, NSTG, ACC16, PRO, SPLIT)
                             ? copy_only_waves<WM, WN, SK, ACC16, PRO, SPLIT>() : 0;
     dim3 grid((unsigned)(a.tiles_m * a.tiles_n * (SPLIT ? a.splits : 1))), block(64 * (WM * WN * SK + NPW));
     // The 8-wave tiles (one k-group) run on 16x16x32 MFMAs, and so do the
-    // four-stage small tiles with fp16 accumulation (use_fast16);
+    // four-stage small tiles in RC (use_fast16);
     // everything else on 32x32x16 (measured per tile: the 16x16x32 kernels
     // of the 4-wave tiles were up to 20% slower with fp32 accumulation, and
     // the 4-wave 256x256 one does not fit its 64 accumulator blocks per wave
     // in registers)
-    if constexpr (use_fast16(LA, LB, BM, BN, WM, WN, SK, NSTG, ACC16, PRO))
+    if constexpr (use_fast16(LA, LB, BM, BN, WM, WN, SK, NSTG, ACC16, PRO, SPLIT))
         hipLaunchKernelGGL((gemm_bias_act_fast16<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, PRO, DUAL, SPLIT>), grid,
                            block, 0, s, a);
     else
