@@ -71,12 +71,19 @@ class GbaError(RuntimeError):
 
 
 def lib():
-    """The loaded library (loaded once).  Raises if it has not been built."""
+    """The loaded library (loaded once).  Raises if it has not been built.
+
+    torch is imported first: its wheel carries its own HIP runtime, which
+    the library then binds to (both name it libamdhip64.so.7).  Loaded
+    before torch, the library would bring in the system's runtime and torch
+    its own beside it: two runtimes in one process, and a launch on one of
+    torch's streams fails."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with "
                                "`python -c 'import __graft_entry__ as g; g.build()'`")
+        import torch  # noqa: F401  (load order: see above)
         L = ctypes.CDLL(LIB_PATH)
         for name, (res, args) in SIGNATURES.items():
             fn = getattr(L, name)

@@ -33,6 +33,27 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(L, name), name
 
 
+def test_library_loaded_before_torch_shares_its_hip_runtime():
+    """The binding loads the library after torch, whatever the caller
+    imported first, so the process holds one HIP runtime (torch's) and the
+    library's launches run on the runtime that owns torch's streams."""
+    import json
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "from paper_2006_12645_amd import gba\n"
+            "gba.lib()\n"
+            "import torch\n"
+            "import json\n"
+            "print(json.dumps(sorted({l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l})))\n"
+            % root)
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+    paths = json.loads(r.stdout.strip().splitlines()[-1])
+    assert len(paths) == 1, paths
+
+
 def gemm(M=64, N=64, K=64, la=0, lb=1, A=FAKE, lda=None, B=FAKE, ldb=None, bias=None, C=FAKE,
          ldc=None, act=1, acc=0, tile=None):
     lda = (K if la == 0 else M) if lda is None else lda
