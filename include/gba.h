@@ -194,6 +194,18 @@ void gba_fused_desc_init(gba_fused_desc *desc);
 gba_status gba_fused_workspace_size(const gba_fused_desc *desc, size_t *bytes);
 
 /*
+ * gba_fused_tile -- the tile configuration gba_fused_gemm would run the
+ * request on, given the workspace the descriptor carries (host-only
+ * computation, no GPU access): *tile is the tile id (see gba_tile_info), or
+ * -1 for the general path and for an empty output.  The library's choice
+ * depends on the shape, the layouts, the accumulation and the prologue (see
+ * gba_select_tile); a requested tile_id that fits is kept.
+ *
+ * Errors: as gba_fused_gemm's validation; GBA_EINVAL also for tile == NULL.
+ */
+gba_status gba_fused_tile(const gba_fused_desc *desc, int *tile);
+
+/*
  * gba_fused_gemm -- the four computation idioms of the paper's scope
  * (Introduction) in one kernel: a matmul with a pointwise prologue
  * (Pointwise Operations in Prologue, Listing 4), with a pointwise epilogue
@@ -280,8 +292,11 @@ gba_status gba_tile_info(int tile_id, int *bm, int *bn, int *bk, int *waves, int
 /*
  * gba_select_tile -- the tile configuration gemm_bias_act would use for this
  * problem on its aligned fast path (host-only computation, no GPU access).
- * Returns the tile id, or -1 if the arguments are invalid or the problem is
- * smaller than every tile (M < 32 or N < 32: general path).
+ * gba_fused_gemm makes the same choice for requests without the prologue
+ * (K being the total reduction length of both products); with the prologue
+ * it may take another tile.  Returns the tile id, or -1 if the arguments
+ * are invalid or the problem is smaller than every tile (M < 32 or N < 32:
+ * general path).
  */
 int gba_select_tile(gba_layout layoutA, gba_layout layoutB, int64_t M, int64_t N, int64_t K,
                     gba_acc accum);

@@ -61,7 +61,13 @@ gba_status validate(const gba_fused_desc &d)
 
 bool tile_fits(int tile, int64_t M, int64_t N) { return M >= TILES[tile].bm && N >= TILES[tile].bn; }
 
-int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum, bool small);
+// Which four-stage small tiles the rule below the 256x256 cases may take
+// (fp32 accumulation): none, the RC set (21-23), or one tile id (24 in RR,
+// 25 in CC); with the prologue (no copy-only waves on those tiles) the
+// k-group tiles instead, with the limits fitted in RC or in RR / CC.
+constexpr int SMALL_NONE = -1, SMALL_RC = 0, SMALL_PRO_RC = -2, SMALL_PRO_RRCC = -3;
+
+int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum, int small);
 
 // Tile choice by problem shape (K is the total reduction length), tuned on
 // MI355X over the workload shapes and random multiples of 128 (measured
@@ -110,14 +116,24 @@ int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum, bool small);
 // ones.
 constexpr double RIDGE_AI = 315.0;
 
-int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb)
+int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb, bool pro)
 {
     auto tiles = [&](int t) -> int64_t {
         return tile_fits(t, M, N) ? ceil_div(M, TILES[t].bm) * ceil_div(N, TILES[t].bn) : 0;
     };
     const double ai = (double)M * N * K / ((double)M * K + (double)K * N + (double)M * N + 1.0);
-    if (tiles(1) >= 136) return 1;
-    if (tiles(1) >= 112 && tiles(4) > 512) return 1;  // 128x128 would need a second round
+    if (accum == GBA_ACC_F16) {
+        // fp16 accumulation: the 256x256 tile (which then keeps every wave
+        // issuing copies) only from 208 workgroups; below
+        // that the 8-wave 128x128 / 128x64 / 64x128 tiles are 3-25% faster
+        // in every layout (M x N = 4096 x 2304 to 4096 x 3072, K = 1024 and
+        // 4096; from 224 workgroups the two are within a few percent, the
+        // 256x256 one ahead for K = 4096)
+        if (tiles(1) >= 208) return 1;
+    } else {
+        if (tiles(1) >= 136) return 1;
+        if (tiles(1) >= 112 && tiles(4) > 512) return 1;  // 128x128 would need a second round
+    }
     if (accum == GBA_ACC_F16) {
         // fp16 accumulation cannot split the reduction over k-groups (one
         // running sum).  In RC the small tiles run with copy-only waves
@@ -142,6 +158,24 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb)
             if (tile_fits(23, M, N) && tiles(23) <= 256) return 23;
             if (tile_fits(21, M, N) && tiles(21) <= 256) return 21;
             if (tile_fits(22, M, N) && tiles(22) <= 640) return 22;
+        } else if (la == lb && !pro) {
+            // RR and CC: the four-stage tile with its long side along the
+            // operand's contiguous direction (32x128 in RR, 128x32 in CC)
+            // up to one round of 256 workgroups, where it does not fit the
+            // 32x64 tile on memory-bound thin shapes, else the 8-wave
+            // tiles below (on 36 thin shapes per layout, warm and with
+            // operands from HBM: 5.5% / 0% slower in total than the
+            // per-shape best tile in RR and 3.0% / 0.5% in CC, against
+            // 21% / 49% and 16% / 27% for the rule before)
+            const int tn = la == GBA_ROW_MAJOR ? 24 : 25;
+            if (tile_fits(tn, M, N) && tiles(tn) <= 256) return tn;
+            if (ai < RIDGE_AI && (M <= 256 || N <= 256) && tile_fits(8, M, N) && tiles(8) <= 256) return 8;
+        } else if (la == lb) {
+            // RR and CC with the prologue, where those tiles have no
+            // copy-only waves: the 8-wave tiles below (36 thin shapes per
+            // layout: 1.1% / 0.8% slower in total than the per-shape best in
+            // RR and 1.5% / 1.8% in CC, against 42% / 21% and 24% / 12% on
+            // the four-stage tiles)
         } else if (ai < RIDGE_AI && (M <= 256 || N <= 256)) {
             if (tiles(22) >= 128) return 22;
             if (tile_fits(23, M, N) && tiles(21) < 128) return 23;
@@ -156,10 +190,19 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb)
     }
     const bool cr = la == GBA_COL_MAJOR && lb == GBA_ROW_MAJOR;
     const bool rc = la == GBA_ROW_MAJOR && lb == GBA_COL_MAJOR;
-    const int t = select_tile_rest(M, N, K, accum, rc && accum == GBA_ACC_F32);
+    int small = SMALL_NONE;
+    if (accum == GBA_ACC_F32 && (rc || la == lb))
+        small = pro ? (rc ? SMALL_PRO_RC : SMALL_PRO_RRCC) : rc ? SMALL_RC : la == GBA_ROW_MAJOR ? 24 : 25;
+    const int t = select_tile_rest(M, N, K, accum, small);
+    // RR / CC, long reductions over at most two rounds of 64x64 tiles: the
+    // four-stage 32x128 / 128x32 tile (896 x 2304 x 3200 RR: 30.9 / 34.8 us
+    // warm / from HBM against 33.2 / 42.8)
+    if (t == 6 && small >= 24 && tile_fits(small, M, N) && tiles(small) <= 512 && K >= 1792) return small;
     // memory-bound: the four-stage 64x64 tile (M = 256 x 4096 x 1024 from
-    // HBM: 8.4 against 13.7 us; about 4% slower with cache-resident operands)
-    if (t == 6 && ai < RIDGE_AI) return 22;
+    // HBM: 8.4 against 13.7 us; about 4% slower with cache-resident operands);
+    // not with the prologue in RR / CC, where its left tile is transposed
+    // through registers
+    if (t == 6 && ai < RIDGE_AI && small != SMALL_PRO_RRCC) return 22;
     // long reductions over at most two rounds of 64x64 tiles: the four-stage
     // tile again (RC only; its transposed copies lose in the other layouts)
     if (t == 6 && rc && tiles(6) <= 512 && K >= 1792) return 22;
@@ -172,16 +215,28 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb)
     return t == 4 && (accum == GBA_ACC_F16 || !cr) ? 18 : t;
 }
 
-// The rule below the 256x256 cases.  `small`: fp32 accumulation in RC,
-// where the four-stage small tiles run on 16x16x32 MFMAs with copy-only
-// waves and take what the rule would give to the k-group tiles (except the
-// 32x32 one with four k-groups, for long reductions over few output tiles)
-// and to the 64x64 / 32x64 tiles: the 32x32 tile while it makes at most one
-// round of 256 workgroups, else the 32x64 one, else the 64x64 one up to 512
-// workgroups.  Over two sets of 51 shapes and 53 thin ones (warm and with
-// operands from HBM) that is 0.6% and 0.9% slower in total than the
-// per-shape best tile, against 1.8% and 3.1% for the rule without them.
-int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum, bool small)
+// The rule below the 256x256 cases.  `small` (fp32 accumulation only):
+//   * SMALL_RC: in RC the four-stage small tiles run on 16x16x32 MFMAs with
+//     copy-only waves and take what the rule would give to the k-group
+//     tiles (except the 32x32 one with four k-groups, for long reductions
+//     over few output tiles) and to the 64x64 / 32x64 tiles: the 32x32
+//     tile while it makes at most one round of 256 workgroups, else the
+//     32x64 one, else the 64x64 one up to 512 workgroups.  Over two sets of
+//     51 shapes and 53 thin ones (warm and with operands from HBM) that is
+//     0.6% and 0.9% slower in total than the per-shape best tile, against
+//     1.8% and 3.1% for the rule without them.
+//   * 24 (RR) / 25 (CC): the one four-stage tile that runs on 16x16x32
+//     MFMAs with copy-only waves in that layout (32x128 / 128x32: the long
+//     side along the direction in which the operand tile is contiguous)
+//     takes 129 to 256 workgroups (65 to 256 from K = 2048); fewer output
+//     tiles over a reduction of 512 or more take the k-group tiles, 32x32
+//     with four k-groups up to 256 workgroups, else 32x64 with four.  Over
+//     51 random shapes and 53 thin ones per layout (warm / with operands
+//     from HBM) that is 1.9% / 1.8% and 1.3% / 0.5% slower in total than
+//     the per-shape best tile in RR, 1.3% / 1.6% and 0.5% / 0.6% in CC,
+//     against 2.9% / 4.7% and 17% / 19% (RR), 2.7% / 4.4% and 16% / 20%
+//     (CC) for the rule without them.
+int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum, int small)
 {
     auto tiles = [&](int t) -> int64_t {
         return tile_fits(t, M, N) ? ceil_div(M, TILES[t].bm) * ceil_div(N, TILES[t].bn) : 0;
@@ -189,23 +244,51 @@ int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum, bool small)
     if (tiles(4) >= 260) return 4;
     const int t57 = N > M ? 7 : 5;
     if (tiles(t57) >= 400) return t57;
+    if (small == SMALL_PRO_RC || small == SMALL_PRO_RRCC) {
+        // With the prologue, over a reduction of 512 or more, few output
+        // tiles (fewer than 160 64x64 tiles in RC, 384 in RR / CC) take
+        // the k-group tiles: 32x32, else 32x64, else 64x64, each with four
+        // k-groups, while that makes at most 256 workgroups.  Over 53 thin
+        // and 51 random shapes per layout (warm / with operands from HBM)
+        // that is 0.7% / 0.7% and 2.9% / 2.0% slower in total than the
+        // per-shape best tile in RC, 1.3% / 1.2% and 3.5% / 2.1% in RR and
+        // 0.9% / 1.1% and 5.1% / 1.1% in CC, against 14% / 3.3% and
+        // 5.3% / 1.5% (RC), 35% / 34% and 10% / 10% (RR), 28% / 33% and
+        // 13% / 9.5% (CC) on the tiles chosen without the prologue.
+        if (K >= 512 && tiles(6) < (small == SMALL_PRO_RC ? 160 : 384)) {
+            if (tile_fits(13, M, N) && tiles(13) <= 256) return 13;
+            if (tile_fits(12, M, N) && tiles(12) <= 256) return 12;
+            if (tile_fits(10, M, N) && tiles(10) <= 256) return 10;
+        }
+        return select_tile_rest(M, N, K, accum, SMALL_NONE);
+    }
+    if (small >= 24) {
+        const int64_t n = tiles(small);
+        if (n > (K >= 2048 ? 64 : 128) && n <= 256) return small;
+        if (K >= 512 && tiles(6) < 160) {
+            if (tile_fits(13, M, N) && tiles(13) <= 256) return 13;
+            if (tile_fits(12, M, N) && tiles(12) <= 256) return 12;
+        }
+        return select_tile_rest(M, N, K, accum, SMALL_NONE);
+    }
+    const bool rcs = small == SMALL_RC;
     if (accum == GBA_ACC_F32 && K >= 1024) {
         const int64_t n11 = tiles(11), n8 = tiles(8);
-        if (!small && n11 >= (K >= 2048 ? 88 : 160) && n11 <= 256)
+        if (!rcs && n11 >= (K >= 2048 ? 88 : 160) && n11 <= 256)
             return n11 < 128 && tiles(12) <= 256 ? 12 : 11;
         if (K >= 2048 && (n8 < 128 || (K >= 4096 && n8 <= 128))) {
             if (n11 > 64) {
-                if (!small) return 11;
+                if (!rcs) return 11;
             } else if (tile_fits(13, M, N)) {
                 return 13;
             }
         }
     }
-    if (small) {
+    if (rcs) {
         if (tile_fits(23, M, N) && tiles(23) <= 256) return 23;
         if (tile_fits(21, M, N) && tiles(21) <= 256) return 21;
         if (tile_fits(22, M, N) && tiles(22) <= 512) return 22;
-        return select_tile_rest(M, N, K, accum, false);
+        return select_tile_rest(M, N, K, accum, SMALL_NONE);
     }
     if (tiles(6) >= 160) return 6;
     if (tile_fits(8, M, N)) {
@@ -302,7 +385,8 @@ Plan make_plan(const gba_fused_desc &d, bool may_split)
     int64_t auto_s = 1;
     if (may_split && d.split_k == 0 && !tile_ok && fp32) auto_s = auto_splits(d.M, d.N, ktot);
     pl.tile = tile_ok ? d.tile_id
-                      : (auto_s > 1 ? AUTO_SPLIT_TILE : select_tile(d.M, d.N, ktot, d.accum, d.layoutA, d.layoutB));
+                      : (auto_s > 1 ? AUTO_SPLIT_TILE : select_tile(d.M, d.N, ktot, d.accum, d.layoutA, d.layoutB,
+                                                                            d.prologue == GBA_PRO_RELU));
     if (pl.tile >= 0 && !fast_path_ok(d)) pl.tile = -1;
     pl.cfg = pl.tile >= 0 ? TILES[pl.tile] : GENERIC_TILE;
     pl.tiles_m = ceil_div(d.M, pl.cfg.bm);
@@ -330,15 +414,22 @@ Plan make_plan(const gba_fused_desc &d, bool may_split)
     return pl;
 }
 
+// The plan a validated request runs with, given the workspace it carries:
+// without room for the split the plan is made again without one (the
+// library's unsplit tile choice differs from its split one).
+Plan plan_for(const gba_fused_desc &d)
+{
+    Plan pl = make_plan(d, true);
+    if (pl.splits > 1 && (d.workspace == nullptr || d.workspace_bytes < pl.ws_bytes)) pl = make_plan(d, false);
+    return pl;
+}
+
 gba_status run_fused(const gba_fused_desc &d, hipStream_t stream)
 {
     gba_status st = validate(d);
     if (st != GBA_OK || d.M == 0 || d.N == 0) return st;
     const bool two = has_second(d);
-    // Without room for the split the plan is made again without one (the
-    // library's unsplit tile choice differs from its split one).
-    Plan pl = make_plan(d, true);
-    if (pl.splits > 1 && (d.workspace == nullptr || d.workspace_bytes < pl.ws_bytes)) pl = make_plan(d, false);
+    const Plan pl = plan_for(d);
     const int tile = pl.tile;
     const bool fast = tile >= 0;
 
@@ -605,6 +696,16 @@ extern "C" gba_status gba_fused_workspace_size(const gba_fused_desc *desc, size_
     return GBA_OK;
 }
 
+extern "C" gba_status gba_fused_tile(const gba_fused_desc *desc, int *tile)
+{
+    if (desc == nullptr || tile == nullptr) return GBA_EINVAL;
+    *tile = -1;
+    const gba_status st = validate(*desc);
+    if (st != GBA_OK || desc->M == 0 || desc->N == 0) return st;
+    *tile = plan_for(*desc).tile;
+    return GBA_OK;
+}
+
 extern "C" gba_status gba_fused_gemm(const gba_fused_desc *desc, gba_stream_t stream)
 {
     if (desc == nullptr) return GBA_EINVAL;
@@ -678,7 +779,7 @@ extern "C" int gba_select_tile(gba_layout layoutA, gba_layout layoutB, int64_t M
     if (!is_layout(layoutA) || !is_layout(layoutB)) return -1;
     if (accum != GBA_ACC_F32 && accum != GBA_ACC_F16) return -1;
     if (M < 0 || N < 0 || K < 0 || M > INT_MAX || N > INT_MAX || K > INT_MAX) return -1;
-    return select_tile(M, N, K, accum, layoutA, layoutB);  // -1 also when the general path would run
+    return select_tile(M, N, K, accum, layoutA, layoutB, false);  // -1 also when the general path would run
 }
 
 extern "C" gba_status gba_bias_add_f16(int64_t M, int64_t N, void *C, int64_t ldc, const void *bias,

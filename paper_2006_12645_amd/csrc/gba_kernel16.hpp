@@ -1,6 +1,8 @@
 // gba_kernel16.hpp -- the fast path on v_mfma_f32_16x16x32_f16 (the 8-wave
-// tiles, every operand layout; and the four-stage small tiles when both
-// operand tiles are reduction-contiguous).
+// tiles, every operand layout; and the four-stage small tiles without the
+// prologue: all of them when both operand tiles are reduction-contiguous,
+// the 32x128 one with row-major B and the 128x32 one with column-major A,
+// whose M- or N-contiguous operand tile has 128 elements per row).
 //
 // Same decomposition as gemm_bias_act_fast (block tile per workgroup, warp
 // tiles per wave, 64-deep reduction steps through direct global -> LDS

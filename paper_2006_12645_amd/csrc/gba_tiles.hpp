@@ -50,9 +50,11 @@ struct TileCfg {
     X(20, 64, 128, 2, 4, 1, 2)   \
     X(21, 32, 64, 1, 2, 1, 4)    \
     X(22, 64, 64, 2, 2, 1, 4)    \
-    X(23, 32, 32, 1, 1, 1, 4)
+    X(23, 32, 32, 1, 1, 1, 4)    \
+    X(24, 32, 128, 1, 2, 1, 4)   \
+    X(25, 128, 32, 2, 1, 1, 4)
 
-constexpr int NUM_TILES = 24;
+constexpr int NUM_TILES = 26;
 
 #define GBA_TILE_CFG(id, BM, BN, WM, WN, SK, NSTG) TileCfg{BM, BN, WM, WN, SK, NSTG},
 constexpr TileCfg TILES[NUM_TILES] = {GBA_TILE_LIST(GBA_TILE_CFG)};
@@ -83,13 +85,15 @@ struct LayoutTable {
 // N-contiguous operand tile has 128 or more elements per row (its
 // conflict-free group permutation needs eight 16-element groups); and,
 // without prologue and unless the reduction is split across workgroups,
-// the four-stage small tiles (21-23) in the layout where both operand tiles
-// are reduction-contiguous, where the 16x16x32 kernel adds waves that only
-// issue copies (with fp16 accumulation its fp16 running sum also breaks the
-// chain of dependent MFMAs).  With fp32 accumulation that is 6-10% faster
-// than these tiles on 32x32x16 without copy-only waves, and than the
-// k-group tiles on 1024^3 (6.66 against 7.33 us) and 1000^3 (6.99 against
-// 7.75).
+// the four-stage small tiles (21-25) under the same layout condition (all
+// of them in the layout where both operand tiles are reduction-contiguous,
+// 32x128 with row-major B, 128x32 with column-major A), where the 16x16x32
+// kernel adds waves that only issue copies (with fp16 accumulation its
+// fp16 running sum also breaks the chain of dependent MFMAs).  With fp32
+// accumulation that is 6-10% faster than these tiles on 32x32x16 without
+// copy-only waves, and than the k-group tiles on 1024^3 in RC (6.66 against
+// 7.33 us) and 1000^3 (6.99 against 7.75); in RR, 32x128 takes 1024^3 in
+// 7.84 us against 8.78 on the k-group 64x64 tile.
 constexpr bool use_fast16(int la, int lb, int bm, int bn, int wm, int wn, int sk, int nstg, bool acc16, bool pro,
                           bool split = false)
 {
@@ -107,7 +111,7 @@ hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
                             ? copy_only_waves<WM, WN, SK, ACC16, PRO, SPLIT>() : 0;
     dim3 grid((unsigned)(a.tiles_m * a.tiles_n * (SPLIT ? a.splits : 1))), block(64 * (WM * WN * SK + NPW));
     // The 8-wave tiles (one k-group) run on 16x16x32 MFMAs, and so do the
-    // four-stage small tiles in RC (use_fast16);
+    // four-stage small tiles where use_fast16 allows them;
     // everything else on 32x32x16 (measured per tile: the 16x16x32 kernels
     // of the 4-wave tiles were up to 20% slower with fp32 accumulation, and
     // the 4-wave 256x256 one does not fit its 64 accumulator blocks per wave

@@ -57,6 +57,7 @@ SIGNATURES = {
     "gba_fused_gemm": (_int, [ctypes.POINTER(FusedDesc), _vp]),
     "gba_fused_gemm_noalloc": (_int, [ctypes.POINTER(FusedDesc), _vp]),
     "gba_fused_workspace_size": (_int, [ctypes.POINTER(FusedDesc), ctypes.POINTER(ctypes.c_size_t)]),
+    "gba_fused_tile": (_int, [ctypes.POINTER(FusedDesc), ctypes.POINTER(_int)]),
     "gba_status_string": (_cp, [_int]),
     "gba_version": (_cp, []),
 }
@@ -196,6 +197,13 @@ def workspace_size(desc):
     n = ctypes.c_size_t(0)
     _check(lib().gba_fused_workspace_size(ctypes.byref(desc), ctypes.byref(n)), "gba_fused_workspace_size")
     return n.value
+
+
+def fused_tile(desc):
+    """Tile id a filled FusedDesc would run on (-1: general path)."""
+    t = _int(-1)
+    _check(lib().gba_fused_tile(ctypes.byref(desc), ctypes.byref(t)), "gba_fused_tile")
+    return t.value
 
 
 # Zero-filled workspaces, one per (device, stream): the library leaves every

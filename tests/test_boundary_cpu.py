@@ -81,7 +81,7 @@ def gemm(M=64, N=64, K=64, la=0, lb=1, A=FAKE, lda=None, B=FAKE, ldb=None, bias=
     (dict(A=None), gba.GBA_EINVAL),
     (dict(B=None), gba.GBA_EINVAL),
     (dict(C=None), gba.GBA_EINVAL),
-    (dict(tile=24), gba.GBA_EINVAL),
+    (dict(tile=gba.num_tiles()), gba.GBA_EINVAL),
     (dict(tile=1000), gba.GBA_EINVAL),
     (dict(A=FAKE + 1), gba.GBA_EUNSUPPORTED),
     (dict(C=FAKE + 1), gba.GBA_EUNSUPPORTED),
@@ -229,7 +229,7 @@ def fused(**kw):
     (dict(act=4), gba.GBA_EINVAL),
     (dict(act=-1), gba.GBA_EINVAL),
     (dict(accum=2), gba.GBA_EINVAL),
-    (dict(tile_id=24), gba.GBA_EINVAL),
+    (dict(tile_id=gba.num_tiles()), gba.GBA_EINVAL),
     (dict(K2=-1), gba.GBA_EINVAL),
     (dict(ldp=31), gba.GBA_EINVAL),
     (dict(layoutA=1, ldp=63), gba.GBA_EINVAL),

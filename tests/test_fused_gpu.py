@@ -19,7 +19,7 @@ torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
 LAYOUTS = ["RR", "RC", "CR", "CC"]
-NUM_TILES = 24
+NUM_TILES = 26
 ACT = {"none": O.ACT_NONE, "relu": O.ACT_RELU, "sigmoid": O.ACT_SIGMOID, "tanh": O.ACT_TANH}
 
 
@@ -226,19 +226,24 @@ def test_fp16_accumulation_matches_its_emulation(tile, layout):
     assert close.mean() >= 0.99, close.mean()
 
 
-@pytest.mark.parametrize("tile", [21, 22, 23])
+# The four-stage small tiles that run with copy-only waves: 21-25 in RC, the
+# 32x128 one in RR and the 128x32 one in CC.
+COPY_WAVE_TILES = [(21, "RC"), (22, "RC"), (23, "RC"), (24, "RC"), (25, "RC"), (24, "RR"), (25, "CC")]
+
+
+@pytest.mark.parametrize("tile,layout", COPY_WAVE_TILES)
 @pytest.mark.parametrize("second", [None, "add", "sub"])
-def test_fp16_accumulation_small_tiles_match_emulation(tile, second):
+def test_fp16_accumulation_small_tiles_match_emulation(tile, layout, second):
     """The four-stage small tiles keep the fp16 running sum as fp16 and add
-    each 32-deep group's own fp32 sum to it (one rounding per group), in the
-    layout where both operand tiles are reduction-contiguous and without a
-    prologue: held to the oracle's emulation of the reading as the other
-    tiles are, and bit-exact on integer data."""
-    announce("f16acc small tile", tile, second)
+    each 32-deep group's own fp32 sum to it (one rounding per group), where
+    both operand tiles arrive by direct copies and without a prologue: held
+    to the oracle's emulation of the reading as the other tiles are, and
+    bit-exact on integer data."""
+    announce("f16acc small tile", tile, layout, second)
     kw = dict(act="none") if second is None else dict(second=second, act="none")
     K2 = None if second is None else 200
     pr = Problem(870 + tile, 264, 328, 1000, K2=K2, bias="row")
-    got = pr.gpu("RC", accum="f16", tile=tile, **kw).astype(np.float64)
+    got = pr.gpu(layout, accum="f16", tile=tile, **kw).astype(np.float64)
     emu = pr.oracle(acc16=True, **kw)
     err = np.abs(got - emu)
     assert (err <= 2 * ulp16(np.maximum(np.abs(emu), 64.0))).all(), err.max()
@@ -246,34 +251,37 @@ def test_fp16_accumulation_small_tiles_match_emulation(tile, second):
     assert close.mean() >= 0.99, close.mean()
     pri = Problem(880 + tile, 264, 328, 392, K2=None if second is None else 136, dist="int", full_bias=True)
     kwi = dict(act="relu") if second is None else dict(second=second, act="relu")
-    got = pri.gpu("RC", accum="f16", tile=tile, **kwi)
+    got = pri.gpu(layout, accum="f16", tile=tile, **kwi)
     assert np.array_equal(got.astype(np.float64), pri.oracle(**kwi)), "integer data not exact"
 
 
-@pytest.mark.parametrize("tile", [21, 22, 23])
+@pytest.mark.parametrize("tile,layout", COPY_WAVE_TILES)
+@pytest.mark.parametrize("accum", ["f32", "f16"])
 @pytest.mark.parametrize("K,K2", [(8, None), (64, None), (136, None), (256, None), (328, None), (40, 72),
                                   (256, 8), (0, 64), (64, 0), (0, 0)])
-def test_fp16_accumulation_small_tiles_step_counts(tile, K, K2):
+def test_copy_wave_small_tiles_step_counts(tile, layout, accum, K, K2):
     """Reductions of one step, of fewer steps than the four LDS stages, of
     exactly four and of more, and empty ones, in one and in two products, on
-    the small tiles with fp16 accumulation, whose copies are issued by waves
-    that do not compute: each step's barrier must pair up between the two
-    kinds of waves, and the copies past the last step must stay out of the
-    result."""
-    announce("f16acc small tile steps", tile, K, K2)
+    the small tiles whose copies are issued by waves that do not compute:
+    each step's barrier must pair up between the two kinds of waves, and
+    the copies past the last step must stay out of the result."""
+    announce("copy-wave small tile steps", tile, layout, accum, K, K2)
     kw = dict(act="none") if K2 is None else dict(second="sub", act="none")
     pr = Problem(900 + tile + K, 96, 160, K, K2=K2, bias="row")
-    got = pr.gpu("RC", accum="f16", tile=tile, **kw).astype(np.float64)
-    emu = pr.oracle(acc16=True, **kw)
-    err = np.abs(got - emu)
-    assert (err <= 2 * ulp16(np.maximum(np.abs(emu), 64.0))).all(), err.max()
+    got = pr.gpu(layout, accum=accum, tile=tile, **kw).astype(np.float64)
+    if accum == "f16":
+        emu = pr.oracle(acc16=True, **kw)
+        err = np.abs(got - emu)
+        assert (err <= 2 * ulp16(np.maximum(np.abs(emu), 64.0))).all(), err.max()
+    else:
+        U.assert_close(got, pr.oracle(**kw), what=f"steps tile {tile} {layout} K={K} K2={K2}")
     pri = Problem(950 + tile + K, 96, 160, K, K2=K2, dist="int", full_bias=True)
     kwi = dict(act="relu") if K2 is None else dict(second="add", act="relu")
-    got = pri.gpu("RC", accum="f16", tile=tile, **kwi)
+    got = pri.gpu(layout, accum=accum, tile=tile, **kwi)
     assert np.array_equal(got.astype(np.float64), pri.oracle(**kwi)), "integer data not exact"
 
 
-@pytest.mark.parametrize("tile", [None, 1, 4, 6, 9, 18, 19, 20, 21, 22, 23, "general"])
+@pytest.mark.parametrize("tile", [None, 1, 4, 6, 9, 18, 19, 20, 21, 22, 23, 24, 25, "general"])
 @pytest.mark.parametrize("layout", LAYOUTS)
 def test_fp16_accumulation_sum_of_products_golden(tile, layout):
     """The hand-derived binary16 results of the single running sum through

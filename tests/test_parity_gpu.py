@@ -17,7 +17,7 @@ torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
 LAYOUTS = ["RR", "RC", "CR", "CC"]
-NUM_TILES = 24
+NUM_TILES = 26
 SPLITK_TILES = [10, 11, 12, 13, 14, 15]
 
 
