@@ -61,11 +61,12 @@ gba_status validate(const gba_fused_desc &d)
 
 bool tile_fits(int tile, int64_t M, int64_t N) { return M >= TILES[tile].bm && N >= TILES[tile].bn; }
 
-// Which four-stage small tiles the rule below the 256x256 cases may take
-// (fp32 accumulation): none, the RC set (21-23), or one tile id (24 in RR,
-// 25 in CC); with the prologue (no copy-only waves on those tiles) the
-// k-group tiles instead, with the limits fitted in RC or in RR / CC.
-constexpr int SMALL_NONE = -1, SMALL_RC = 0, SMALL_PRO_RC = -2, SMALL_PRO_RRCC = -3;
+// Which small tiles the rule below the 256x256 cases may take (fp32
+// accumulation): none, the RC set of four-stage tiles (21-23), or one tile
+// id (24 in RR, 25 in CC); where no four-stage tile has copy-only waves
+// (the prologue, and the CR layout) the k-group tiles instead, with the
+// limits fitted in RC (SMALL_PRO_RC) or in the other layouts (SMALL_KGROUP).
+constexpr int SMALL_NONE = -1, SMALL_RC = 0, SMALL_PRO_RC = -2, SMALL_KGROUP = -3;
 
 int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum, int small);
 
@@ -176,11 +177,24 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb, bool
             // layout: 1.1% / 0.8% slower in total than the per-shape best in
             // RR and 1.5% / 1.8% in CC, against 42% / 21% and 24% / 12% on
             // the four-stage tiles)
-        } else if (ai < RIDGE_AI && (M <= 256 || N <= 256)) {
-            if (tiles(22) >= 128) return 22;
-            if (tile_fits(23, M, N) && tiles(21) < 128) return 23;
-            if (tile_fits(21, M, N)) return 21;
-            if (tile_fits(23, M, N)) return 23;
+        } else {
+            // CR, where no small tile has copy-only waves: thin memory-bound
+            // shapes take the two-stage 32x32 tile (at most 512 workgroups,
+            // at most 128 rows or columns), else 64x64 up to 512
+            // workgroups; then 128x128 from 384 workgroups, else the 8-wave
+            // tile with its long side along the longer output side (on 36
+            // thin and 51 random shapes, warm / with operands from HBM:
+            // 1.4% / 0.4% and 1.4% / 1.6% slower in total than the
+            // per-shape best tile, against 6.3% / 2.5% and 4.6% / 5.0%; with
+            // the prologue, thin: 1.2% / 0.5% against 11% / 5.5%)
+            if (ai < RIDGE_AI && (M <= 256 || N <= 256)) {
+                if (tile_fits(9, M, N) && tiles(9) <= 512 && (M < N ? M : N) <= 128) return 9;
+                if (tile_fits(6, M, N) && tiles(6) <= 512) return 6;
+            }
+            if (tiles(18) >= 384) return 18;
+            const int t8w = N > M ? 20 : 19;
+            if (tile_fits(t8w, M, N)) return t8w;
+            if (tiles(18) >= 128) return 18;
         }
         const int64_t t18 = tiles(18);
         if (t18 >= 384 || (t18 >= 128 && t18 < 256 && K <= 1024)) return 18;
@@ -191,8 +205,10 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb, bool
     const bool cr = la == GBA_COL_MAJOR && lb == GBA_ROW_MAJOR;
     const bool rc = la == GBA_ROW_MAJOR && lb == GBA_COL_MAJOR;
     int small = SMALL_NONE;
-    if (accum == GBA_ACC_F32 && (rc || la == lb))
-        small = pro ? (rc ? SMALL_PRO_RC : SMALL_PRO_RRCC) : rc ? SMALL_RC : la == GBA_ROW_MAJOR ? 24 : 25;
+    if (accum == GBA_ACC_F32) {
+        if (cr) small = SMALL_KGROUP;
+        else small = pro ? (rc ? SMALL_PRO_RC : SMALL_KGROUP) : rc ? SMALL_RC : la == GBA_ROW_MAJOR ? 24 : 25;
+    }
     const int t = select_tile_rest(M, N, K, accum, small);
     // RR / CC, long reductions over at most two rounds of 64x64 tiles: the
     // four-stage 32x128 / 128x32 tile (896 x 2304 x 3200 RR: 30.9 / 34.8 us
@@ -200,9 +216,9 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb, bool
     if (t == 6 && small >= 24 && tile_fits(small, M, N) && tiles(small) <= 512 && K >= 1792) return small;
     // memory-bound: the four-stage 64x64 tile (M = 256 x 4096 x 1024 from
     // HBM: 8.4 against 13.7 us; about 4% slower with cache-resident operands);
-    // not with the prologue in RR / CC, where its left tile is transposed
-    // through registers
-    if (t == 6 && ai < RIDGE_AI && small != SMALL_PRO_RRCC) return 22;
+    // not in CR or with the prologue in RR / CC, where it has no copy-only
+    // waves and a transposed tile
+    if (t == 6 && ai < RIDGE_AI && small != SMALL_KGROUP) return 22;
     // long reductions over at most two rounds of 64x64 tiles: the four-stage
     // tile again (RC only; its transposed copies lose in the other layouts)
     if (t == 6 && rc && tiles(6) <= 512 && K >= 1792) return 22;
@@ -244,17 +260,20 @@ int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum, int small)
     if (tiles(4) >= 260) return 4;
     const int t57 = N > M ? 7 : 5;
     if (tiles(t57) >= 400) return t57;
-    if (small == SMALL_PRO_RC || small == SMALL_PRO_RRCC) {
-        // With the prologue, over a reduction of 512 or more, few output
-        // tiles (fewer than 160 64x64 tiles in RC, 384 in RR / CC) take
-        // the k-group tiles: 32x32, else 32x64, else 64x64, each with four
-        // k-groups, while that makes at most 256 workgroups.  Over 53 thin
-        // and 51 random shapes per layout (warm / with operands from HBM)
-        // that is 0.7% / 0.7% and 2.9% / 2.0% slower in total than the
-        // per-shape best tile in RC, 1.3% / 1.2% and 3.5% / 2.1% in RR and
-        // 0.9% / 1.1% and 5.1% / 1.1% in CC, against 14% / 3.3% and
+    if (small == SMALL_PRO_RC || small == SMALL_KGROUP) {
+        // With the prologue, and in CR, over a reduction of 512 or more,
+        // few output tiles (fewer than 160 64x64 tiles in RC, 384 in the
+        // other layouts) take the k-group tiles: 32x32, else 32x64, else
+        // 64x64, each with four k-groups, while that makes at most 256
+        // workgroups.  With the prologue, over 53 thin and 51 random shapes
+        // per layout (warm / with operands from HBM) that is 0.7% / 0.7% and
+        // 2.9% / 2.0% slower in total than the per-shape best tile in RC,
+        // 1.3% / 1.2% and 3.5% / 2.1% in RR, 0.9% / 1.1% and 5.1% / 1.1% in
+        // CC and 1.2% / 0.6% and 2.4% / 3.0% in CR, against 14% / 3.3% and
         // 5.3% / 1.5% (RC), 35% / 34% and 10% / 10% (RR), 28% / 33% and
-        // 13% / 9.5% (CC) on the tiles chosen without the prologue.
+        // 13% / 9.5% (CC), 9.8% / 14% and 2.8% / 3.6% (CR) on the tiles
+        // chosen without it; CR without the prologue 1.0% / 0.5% and
+        // 2.7% / 4.0%, against 8.6% / 14% and 3.0% / 4.6%.
         if (K >= 512 && tiles(6) < (small == SMALL_PRO_RC ? 160 : 384)) {
             if (tile_fits(13, M, N) && tiles(13) <= 256) return 13;
             if (tile_fits(12, M, N) && tiles(12) <= 256) return 12;

@@ -59,10 +59,21 @@ def test_prologue_never_takes_copy_wave_tiles(layout, accum):
     on waves of their own only without the prologue; with it they were the
     slowest of the small tiles, so the rule does not give them a request
     with the prologue."""
-    banned = {24, 25} | ({21, 23} if accum == "f32" and layout != "CR" else set())
+    banned = {24, 25} | ({21, 23} if accum == "f32" or layout == "CR" else set())
     for M, N, K in shapes(12, 300):
         t = gba.fused_tile(desc(M, N, K, layout, accum, prologue=True))
         assert t not in banned or (layout == "RC" and accum == "f16"), (M, N, K, t)
+
+
+@pytest.mark.parametrize("accum", ACCS)
+@pytest.mark.parametrize("prologue", [False, True])
+def test_cr_never_takes_four_stage_small_tiles(accum, prologue):
+    """In CR no small four-stage tile has copy-only waves (both operand
+    tiles are M- or N-contiguous and shorter than 128 elements per row), and
+    the two-stage and k-group tiles were faster there."""
+    for M, N, K in shapes(13, 300):
+        t = gba.fused_tile(desc(M, N, K, "CR", accum, prologue=prologue))
+        assert t not in {21, 23, 24, 25}, (M, N, K, t)
 
 
 @pytest.mark.parametrize("case,tile", [
@@ -85,6 +96,16 @@ def test_prologue_never_takes_copy_wave_tiles(layout, accum):
     # 256x256 tile, 172.4 / 162.7 against 170.3 / 176.6
     (dict(M=4096, N=3072, K=4096, accum="f16"), 18),
     (dict(M=4096, N=4096, K=4096, accum="f16"), 1),
+    # CR, fp32: 64x64 with four k-groups on 1024^3, 9.09 / 11.38 against
+    # 9.19 / 11.81 with two; 128 x 4096 x 2048 on 32x64 with four k-groups
+    # 12.29 / 16.88 against 13.10 / 22.74 on 64x64 with two
+    (dict(M=1024, N=1024, K=1024, layout="CR"), 10),
+    (dict(M=128, N=4096, K=2048, layout="CR"), 12),
+    # CR, fp16: 32 x 4096 x 1024 on the two-stage 32x32 tile 10.71 / 16.89
+    # against 11.54 / 17.12 on the four-stage one; 1280 x 2816 x 3968 on the
+    # 8-wave 64x128 tile 57.82 / 64.32 against 62.62 / 72.91 on 128x128
+    (dict(M=32, N=4096, K=1024, layout="CR", accum="f16"), 9),
+    (dict(M=1280, N=2816, K=3968, layout="CR", accum="f16"), 20),
     # a requested tile that fits is kept
     (dict(M=1024, N=1024, K=1024, layout="RR", prologue=True, tile=24), 24),
 ])
