@@ -437,6 +437,24 @@ def test_large_leading_dimensions(layout, ld):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("tile,layout", COPY_WAVE_TILES)
+@pytest.mark.parametrize("ld", [FAST_MAX_LD - 8, FAST_MAX_LD])
+def test_large_leading_dimensions_copy_wave_tiles(tile, layout, ld):
+    """The small tiles whose copies run on waves of their own (no prologue),
+    with both products at the fast path's largest leading dimension and
+    just past it."""
+    pr = Problem(835, 300, 264, 264, K2=136, full_bias=True)
+    kw = dict(second="sub", bias_op="sub", act="relu")
+    ref = pr.oracle(**kw)
+    big = torch.full((pr.M, FAST_MAX_LD + 8), float("nan"), dtype=torch.float16, device="cuda")
+    out = big[:, :pr.N]
+    announce("large_ld copy waves", tile, layout, ld)
+    U.assert_close(pr.gpu(layout, **kw, tile=tile, ld=ld, out=out), ref, what=f"ld={ld} {layout} tile {tile}")
+    assert torch.isnan(big[:, pr.N:pr.N + 64]).all().item()
+    del big, out
+    torch.cuda.empty_cache()
+
+
 # ----------------------------------------------------------------------------
 # Reduction split across workgroups (partials in a workspace, summed by the
 # last split of each tile)
@@ -452,7 +470,7 @@ def counters_zero(ws, tile, M, N):
     return not ws[:tiles * 4].any().item()
 
 
-@pytest.mark.parametrize("tile", [4, 5, 6, 7, 8, 9, 18, 19, 20])
+@pytest.mark.parametrize("tile", [4, 5, 6, 7, 8, 9, 18, 19, 20, 21, 22, 23, 24, 25])
 @pytest.mark.parametrize("split", [2, 3, 7])
 def test_split_reduction_all_features(tile, split):
     # 16 + 4 steps of A.B and P.Q, ragged output (shifted edge tiles)
