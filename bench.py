@@ -44,14 +44,40 @@ HEADLINE = "cube4096_RC"
 PROFILES = os.path.join(ROOT, "profiles")
 
 
+def strip_comments(src):
+    """C++ source without its comments and with runs of whitespace collapsed
+    (string and character literals are kept as they are)."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if c in "\"'":
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        elif src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            out.append(" ")
+            i = n if j < 0 else j + 2
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_digest():
-    """sha256 over the HIP sources, to tell whether stored counters are stale."""
+    """sha256 over the HIP sources with their comments removed, to tell
+    whether stored counters were taken on the code that is built now."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2006_12645_amd", "csrc")
     for name in sorted(os.listdir(csrc)):
         if name.endswith((".hip", ".hpp")):
             h.update(name.encode())
-            h.update(open(os.path.join(csrc, name), "rb").read())
+            h.update(strip_comments(open(os.path.join(csrc, name), encoding="utf-8").read()).encode())
     return h.hexdigest()
 
 

@@ -70,9 +70,12 @@ constexpr int SMALL_NONE = -1, SMALL_RC = 0, SMALL_PRO_RC = -2, SMALL_KGROUP = -
 
 int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum, int small);
 
-// Tile choice by problem shape (K is the total reduction length), tuned on
-// MI355X over the workload shapes and random multiples of 128 (measured
-// sweeps of every tile, RC layout, fp32 accumulation):
+// Tile choice by problem shape (K is the total reduction length), the
+// operand layouts, the accumulation and the prologue, tuned on MI355X over
+// the workload shapes, random multiples of 128 and thin shapes (measured
+// sweeps of every tile, warm and with operands from HBM).  The base rule
+// (fitted in RC with fp32 accumulation; the layout-, accumulation- and
+// prologue-specific branches are described where they are taken):
 //   * the 256x256 tile (8 waves) as soon as it yields 136 workgroups: one
 //     round over 53% or more of the 256 compute units beats two rounds of
 //     a smaller tile; from 112 when 128x128 tiles (two per compute unit)
@@ -93,27 +96,25 @@ int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum, int small);
 //     stages;
 //   * else 64x64 from 160 workgroups (in RC, the four-stage 64x64 tile
 //     instead for K >= 1792 over at most 512 of them), then 32x64 --
-//     replaced, for fp32
-//     accumulation and K >= 768, by 32x32 with four k-groups when that
-//     makes at most 128 workgroups, else by 32x64 with four k-groups when
-//     that makes at most 256 -- then 32x32.
+//     replaced, for fp32 accumulation and K >= 768, by 32x32 with four
+//     k-groups when that makes at most 128 workgroups, else by 32x64 with
+//     four k-groups when that makes at most 256 -- then 32x32.
 // The 256x128 and 128x256 tiles (4 or 8 waves) were never clearly the
 // fastest in those sweeps and are only used when asked for.  128x128 means
 // the 8-wave tile on 16x16x32 MFMAs: with fp32 accumulation 3-6% faster
 // than the 4-wave one over the shapes the rule gives it, except with
 // column-major A and row-major B, where the two were within a few percent
 // either way.  Over four sets of 51 shapes in RC (two of them held out from
-// the fitting) the rule is 0.35-0.5% slower in total than the per-shape
-// best tile (1.3-1.5% before the 8-wave 128x64 / 64x128 tiles and the
-// four-stage 64x64 one took the shapes above); over one set each, 2.1% in
-// RR, 1.0% in CC and 4.2% in CR.  With
-// fp16 accumulation the 8-wave tiles are 25-40% faster than the 4-wave
-// ones from 128x128 down and about 10% faster than 64x64 or 32x64 on the
+// the fitting) the base rule is 0.35-0.5% slower in total than the
+// per-shape best tile (1.3-1.5% before the 8-wave 128x64 / 64x128 tiles
+// and the four-stage 64x64 one took the shapes above).  With fp16
+// accumulation the 8-wave tiles are 25-40% faster than the 4-wave ones
+// from 128x128 down and about 10% faster than 64x64 or 32x64 on the
 // small-M inference shapes (measured in the RC layout), so they come first.
 // Flops per byte of compulsory traffic (2MNK over 2(MK + KN + MN)) at the
 // ridge point of the part (2500 TFLOP/s over 8 TB/s): below it a problem
 // is bound by HBM when its operands come from there, and the four-stage
-// tiles (21-23: copies three steps ahead of the MFMAs) beat the two-stage
+// tiles (21-25: copies three steps ahead of the MFMAs) beat the two-stage
 // ones.
 constexpr double RIDGE_AI = 315.0;
 

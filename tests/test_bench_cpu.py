@@ -49,3 +49,10 @@ def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
                        text=True, timeout=300, cwd=ROOT)
     assert r.returncode != 0 and "one GPU" in r.stderr, (r.returncode, r.stderr[-500:])
+
+
+def test_source_digest_ignores_comments_only():
+    src = 'int a = 1; // note\n/* block\n   note */ const char *s = "x // y /* z */";\nint  b;'
+    assert bench.strip_comments(src) == 'int a = 1; const char *s = "x // y /* z */"; int b;'
+    assert bench.strip_comments(src.replace("note", "other note")) == bench.strip_comments(src)
+    assert bench.strip_comments(src.replace("b;", "c;")) != bench.strip_comments(src)
