@@ -146,10 +146,8 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb, bool
         // operands from HBM: 1.1% and 0.4% slower in total than the
         // per-shape best tile, against 4.9% and 16% for the rule before;
         // the 8-wave tiles keep two stages and pull less from HBM: 896 x
-        // 1536 x 1024, 15.6 against 11.8 us cold).  Larger problems, and
-        // thin memory-bound ones in the other layouts (the four-stage tiles
-        // there, measured on M = 32 / 128 / 256 x 4096 x 1024 and 1000^3:
-        // 13-19 us on the two-stage tiles against 11-12.5), then the 8-wave
+        // 1536 x 1024, 15.6 against 11.8 us cold).  The other layouts have
+        // branches of their own below.  Larger problems then take the 8-wave
         // tiles on 16x16x32 MFMAs (their two waves per SIMD overlap one
         // wave's rounding with the other's MFMAs): 128x128 for one round of
         // short reductions (K <= 1024, 128-255 workgroups) and from 384
