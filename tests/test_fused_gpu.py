@@ -168,11 +168,12 @@ def test_everything_at_once(layout):
 # Every tile, and fp16 accumulation
 
 @pytest.mark.parametrize("tile", range(NUM_TILES))
-def test_every_tile_all_features(tile):
-    announce("tile", tile)
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_every_tile_all_features(tile, layout):
+    announce("tile all features", tile, layout)
     pr = Problem(760, 520, 392, 264, K2=200, full_bias=True)
     kw = dict(prologue=True, second="sub", bias_op="add", act="relu")
-    U.assert_close(pr.gpu("RC", **kw, tile=tile), pr.oracle(**kw), what=f"tile {tile}")
+    U.assert_close(pr.gpu(layout, **kw, tile=tile), pr.oracle(**kw), what=f"tile {tile} {layout}")
 
 
 @pytest.mark.parametrize("tile", [1, 16, 17, 18, 19, 20])
