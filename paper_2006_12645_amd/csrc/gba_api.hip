@@ -272,7 +272,10 @@ int select_tile_rest(int64_t M, int64_t N, int64_t K, int accum, int small)
         // 5.3% / 1.5% (RC), 35% / 34% and 10% / 10% (RR), 28% / 33% and
         // 13% / 9.5% (CC), 9.8% / 14% and 2.8% / 3.6% (CR) on the tiles
         // chosen without it; CR without the prologue 1.0% / 0.5% and
-        // 2.7% / 4.0%, against 8.6% / 14% and 3.0% / 4.6%.
+        // 2.7% / 4.0%, against 8.6% / 14% and 3.0% / 4.6%.  Held out (51
+        // random shapes, seed 4242, with the prologue): RC 2.8% / 2.1%, RR
+        // 3.3% / 2.8%, CC 4.0% / 1.4%, against 4.1% / 1.7%, 9.1% / 9.3% and
+        // 11% / 8.5% ignoring the prologue.
         if (K >= 512 && tiles(6) < (small == SMALL_PRO_RC ? 160 : 384)) {
             if (tile_fits(13, M, N) && tiles(13) <= 256) return 13;
             if (tile_fits(12, M, N) && tiles(12) <= 256) return 12;
