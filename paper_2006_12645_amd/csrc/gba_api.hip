@@ -751,6 +751,7 @@ extern "C" gba_status gba_fused_gemm_noalloc(const gba_fused_desc *desc, gba_str
         // earlier call left behind.
         const int64_t ntiles = pl.tiles_m * pl.tiles_n;
         hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        clear_last_error();
         hipLaunchKernelGGL(zero_words_kernel, dim3((unsigned)ceil_div(ntiles, 256)), dim3(256), 0, s,
                            static_cast<unsigned *>(ws), (int)ntiles);
         if (hipGetLastError() != hipSuccess) return GBA_EHIP;
@@ -813,6 +814,7 @@ extern "C" gba_status gba_bias_add_f16(int64_t M, int64_t N, void *C, int64_t ld
     dim3 grid(pointwise_grid(M, N)), block(256);
     _Float16 *c = static_cast<_Float16 *>(C);
     const _Float16 *b = static_cast<const _Float16 *>(bias);
+    clear_last_error();
     if (vec)
         hipLaunchKernelGGL(bias_add_kernel<true>, grid, block, 0, s, c, ldc, b, (int)M, (int)N);
     else
@@ -831,6 +833,7 @@ extern "C" gba_status gba_bias_act_f16(int64_t M, int64_t N, void *C, int64_t ld
     dim3 grid(pointwise_grid(M, N)), block(256);
     _Float16 *c = static_cast<_Float16 *>(C);
     const _Float16 *b = static_cast<const _Float16 *>(bias);
+    clear_last_error();
     if (vec)
         hipLaunchKernelGGL(bias_act_kernel<true>, grid, block, 0, s, c, ldc, b, (int)act, (int)M, (int)N);
     else
@@ -846,6 +849,7 @@ extern "C" gba_status gba_relu_f16(int64_t M, int64_t N, void *C, int64_t ldc, g
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     dim3 grid(pointwise_grid(M, N)), block(256);
     _Float16 *c = static_cast<_Float16 *>(C);
+    clear_last_error();
     if (vec)
         hipLaunchKernelGGL(relu_kernel<true>, grid, block, 0, s, c, ldc, (int)M, (int)N);
     else
@@ -864,6 +868,7 @@ extern "C" gba_status gba_add_f16(int64_t M, int64_t N, void *C, int64_t ldc, co
     dim3 grid(pointwise_grid(M, N)), block(256);
     _Float16 *c = static_cast<_Float16 *>(C);
     const _Float16 *x = static_cast<const _Float16 *>(X);
+    clear_last_error();
     if (vec)
         hipLaunchKernelGGL(add_kernel<true>, grid, block, 0, s, c, ldc, x, ldx, (int)M, (int)N);
     else

@@ -102,6 +102,12 @@ constexpr bool use_fast16(int la, int lb, int bm, int bn, int wm, int wn, int sk
     return (acc16 || !split) && !pro && sk == 1 && nstg == 4 && layouts;
 }
 
+// hipGetLastError reports the last failure of any runtime call on the
+// calling thread, not only of the launch before it: the launchers clear it
+// first, so that an earlier, unrelated failure does not turn a kernel that
+// was enqueued (and will run) into an error return.
+inline void clear_last_error() { (void)hipGetLastError(); }
+
 template <int BM, int BN, int WM, int WN, int SK, int NSTG, int LA, int LB, bool ACC16, bool PRO, bool DUAL,
           bool SPLIT = false>
 hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
@@ -116,6 +122,7 @@ hipError_t launch_fast(const GemmArgs &a, hipStream_t s)
     // of the 4-wave tiles were up to 20% slower with fp32 accumulation, and
     // the 4-wave 256x256 one does not fit its 64 accumulator blocks per wave
     // in registers)
+    clear_last_error();
     if constexpr (use_fast16(LA, LB, BM, BN, WM, WN, SK, NSTG, ACC16, PRO, SPLIT))
         hipLaunchKernelGGL((gemm_bias_act_fast16<BM, BN, WM, WN, SK, NSTG, LA, LB, ACC16, PRO, DUAL, SPLIT>), grid,
                            block, 0, s, a);
@@ -147,6 +154,7 @@ hipError_t launch_generic(const GemmArgs &a, hipStream_t s)
 {
     constexpr TileCfg c = GENERIC_TILE;
     dim3 grid((unsigned)(a.tiles_m * a.tiles_n)), block(64 * c.wm * c.wn);
+    clear_last_error();
     hipLaunchKernelGGL((gemm_bias_act_generic<c.bm, c.bn, c.wm, c.wn, LA, LB, ACC16, PRO, DUAL>),
                        grid, block, 0, s, a);
     return hipGetLastError();

@@ -100,6 +100,37 @@ class Problem:
 
 
 # ----------------------------------------------------------------------------
+def test_earlier_runtime_failure_does_not_fail_a_launch():
+    """A failed runtime call made earlier on the same thread (hipSetDevice
+    with a device index that does not exist: rejected on the host, nothing
+    reaches the GPU) leaves the thread's last error set; the library's
+    launches must neither report it as their own nor skip their work, and
+    they leave it cleared.  The operands are on the device before the
+    failed call, so that only the library runs between it and the check."""
+    import ctypes
+    announce("stale runtime error")
+    hip = gba.lib()  # resolves the runtime's own symbols through the library's dependencies
+    hip.hipSetDevice.argtypes = [ctypes.c_int]
+    hip.hipSetDevice.restype = ctypes.c_int
+    hip.hipGetLastError.restype = ctypes.c_int
+    pr = Problem(705, 264, 136, 200)
+    A, B = U.device_operand(pr.A, D.ROW), U.device_operand(pr.B, D.COL)
+    bias = torch.from_numpy(pr.bias).cuda()
+    out = torch.empty((pr.M, pr.N), dtype=torch.float16, device="cuda")
+    C = torch.from_numpy(D.uniform_f16(706, (64, 72), -1, 1)).cuda()
+    want_relu = np.maximum(C.cpu().numpy(), 0)
+    torch.cuda.synchronize()
+    assert hip.hipSetDevice(1 << 20) != 0
+    gba.fused_gemm(A, B, bias=bias, out=out)
+    assert hip.hipGetLastError() == 0
+    assert hip.hipSetDevice(1 << 20) != 0
+    gba.relu_(C)
+    assert hip.hipGetLastError() == 0
+    torch.cuda.synchronize()
+    U.assert_close(out.cpu().numpy(), pr.oracle(), what="fused after a failed runtime call")
+    assert np.array_equal(C.cpu().numpy(), want_relu)
+
+
 # Each idiom in all layouts, several tiles plus a ragged tail on the fast path
 
 @pytest.mark.parametrize("layout", LAYOUTS)
