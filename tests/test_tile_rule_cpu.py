@@ -106,6 +106,10 @@ def test_cr_never_takes_four_stage_small_tiles(accum, prologue):
     # 8-wave 64x128 tile 57.82 / 64.32 against 62.62 / 72.91 on 128x128
     (dict(M=32, N=4096, K=1024, layout="CR", accum="f16"), 9),
     (dict(M=1280, N=2816, K=3968, layout="CR", accum="f16"), 20),
+    # RC, fp32, 64 x 4096 x 2048 (128 32x64 tiles): 32x32 with four
+    # k-groups 7.58 / 9.07 against 7.38 / 10.58 on the four-stage 32x32 tile
+    (dict(M=64, N=4096, K=2048), 13),
+    (dict(M=64, N=4096, K=1024), 23),
     # a requested tile that fits is kept
     (dict(M=1024, N=1024, K=1024, layout="RR", prologue=True, tile=24), 24),
 ])
