@@ -348,9 +348,11 @@ def test_deterministic_and_stream():
 
 def test_graph_capture_replays():
     """The fused kernels captured in a HIP graph (a plain call, a call with
-    the reduction split across workgroups through a caller workspace, and
-    the transposed layout) replay to the eager results, replay after replay,
-    with eager work of the library on the same buffers in between."""
+    the reduction split across workgroups through a caller workspace, the
+    transposed layout, and two small tiles whose copies run on waves of
+    their own, one with fp16 accumulation) replay to the eager results,
+    replay after replay, with eager work of the library on the same buffers
+    in between."""
     announce("graph capture")
     M, N, K = 384, 256, 4096
     A, B, bias = D.random_problem(69, M, N, K)
@@ -358,10 +360,12 @@ def test_graph_capture_replays():
     dAc, dBr = U.device_operand(A, D.COL), U.device_operand(B, D.ROW)
     dbias = torch.from_numpy(bias).cuda()
     ws = torch.zeros(16 << 20, dtype=torch.uint8, device="cuda")
-    outs = [torch.empty(M, N, dtype=torch.float16, device="cuda") for _ in range(3)]
+    outs = [torch.empty(M, N, dtype=torch.float16, device="cuda") for _ in range(5)]
     calls = [lambda: gba.gemm_bias_act(dA, dB, dbias, out=outs[0]),
              lambda: gba.fused_gemm(dA, dB, bias=dbias, tile=6, split=8, workspace=ws, out=outs[1]),
-             lambda: gba.fused_gemm(dAc, dBr, bias=dbias, act="tanh", out=outs[2])]
+             lambda: gba.fused_gemm(dAc, dBr, bias=dbias, act="tanh", out=outs[2]),
+             lambda: gba.fused_gemm(dA, dBr, bias=dbias, tile=24, out=outs[3]),
+             lambda: gba.fused_gemm(dA, dB, bias=dbias, tile=21, accum="f16", out=outs[4])]
     for f in calls:
         f()
     torch.cuda.synchronize()
