@@ -113,19 +113,41 @@ def _stream_handle(stream, device):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def _stored_as(t, rows, cols, layout):
+    """Whether a 2-D tensor holding a logical rows x cols matrix can be
+    passed in `layout` (a single row or column fits either layout)."""
+    s0, s1 = t.stride()
+    if layout == GBA_ROW_MAJOR:
+        return (s1 == 1 or cols <= 1) and (rows <= 1 or s0 >= cols)
+    return (s0 == 1 or rows <= 1) and (cols <= 1 or s1 >= rows)
+
+
 def operand_layout(t, rows, cols, want=None):
     """(layout, ld) of a 2-D tensor holding a logical rows x cols matrix;
     ``want`` asks for that layout (for operands that must match another)."""
     if t.dim() != 2 or tuple(t.shape) != (rows, cols):
         raise ValueError(f"expected a {rows}x{cols} matrix, got shape {tuple(t.shape)}")
     s0, s1 = t.stride()
-    if want in (None, GBA_ROW_MAJOR) and (s1 == 1 or cols <= 1) and (rows <= 1 or s0 >= cols):
+    if want in (None, GBA_ROW_MAJOR) and _stored_as(t, rows, cols, GBA_ROW_MAJOR):
         return GBA_ROW_MAJOR, (s0 if rows > 1 else max(cols, 1))
-    if want in (None, GBA_COL_MAJOR) and (s0 == 1 or rows <= 1) and (cols <= 1 or s1 >= rows):
+    if want in (None, GBA_COL_MAJOR) and _stored_as(t, rows, cols, GBA_COL_MAJOR):
         return GBA_COL_MAJOR, (s1 if cols > 1 else max(rows, 1))
     if want is not None:
         raise ValueError("P and Q must be stored in the layouts of A and B")
     raise ValueError("operand must be row- or column-major (one unit stride)")
+
+
+def shared_layout(x, rows, cols, y, rows2, cols2):
+    """The layout two operands that must share one (A and P, or B and Q)
+    are passed in: row-major if both can be, else column-major.  An operand
+    with a single row or column fits either, so the other one decides."""
+    for t, r, c in ((x, rows, cols), (y, rows2, cols2)):
+        if t.dim() != 2 or tuple(t.shape) != (r, c):
+            raise ValueError(f"expected a {r}x{c} matrix, got shape {tuple(t.shape)}")
+    for layout in (GBA_ROW_MAJOR, GBA_COL_MAJOR):
+        if _stored_as(x, rows, cols, layout) and _stored_as(y, rows2, cols2, layout):
+            return layout
+    raise ValueError("P and Q must be stored in the layouts of A and B")
 
 
 def _row_major_ld(t, what):
@@ -291,11 +313,13 @@ def fused_gemm(A, B, *, P=None, Q=None, second="add", prologue=None, bias=None, 
     # Layouts come from the operands that are read; an empty reduction's
     # operands are never read, so their layout and leading dimension are
     # free (the smallest legal ones are passed).
+    want_a = want_b = None
+    if K > 0 and K2 > 0:
+        want_a, want_b = shared_layout(A, M, K, P, M, K2), shared_layout(B, K, N, Q, K2, N)
     if K > 0:
-        d.layoutA, d.lda = operand_layout(A, M, K)
-        d.layoutB, d.ldb = operand_layout(B, K, N)
+        d.layoutA, d.lda = operand_layout(A, M, K, want=want_a)
+        d.layoutB, d.ldb = operand_layout(B, K, N, want=want_b)
     if K2 > 0:
-        want_a, want_b = (d.layoutA, d.layoutB) if K > 0 else (None, None)
         d.layoutA, d.ldp = operand_layout(P, M, K2, want=want_a)
         d.layoutB, d.ldq = operand_layout(Q, K2, N, want=want_b)
     row_a, row_b = d.layoutA == GBA_ROW_MAJOR, d.layoutB == GBA_ROW_MAJOR

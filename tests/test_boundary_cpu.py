@@ -408,3 +408,22 @@ def test_noalloc_rejects_a_split_beyond_its_scratch():
     d.M = -1
     assert L.gba_fused_gemm_noalloc(ctypes.byref(d), None) == gba.GBA_EINVAL
     assert L.gba_fused_gemm_noalloc(None, None) == gba.GBA_EINVAL
+
+
+def test_shared_layout_of_a_and_p():
+    """A and P (and B and Q) are passed in one layout; an operand with a
+    single row or column fits either, so the other one decides, and two
+    operands stored in different layouts are refused."""
+    torch = pytest.importorskip("torch")
+    row = lambda r, c, ld: torch.empty(r, ld, dtype=torch.float16)[:, :c]
+    col = lambda r, c, ld: torch.empty(c, ld, dtype=torch.float16)[:, :r].t()
+    R, C = gba.GBA_ROW_MAJOR, gba.GBA_COL_MAJOR
+    # K = 1: A (48 x 1) is a single column, P decides
+    assert gba.shared_layout(col(48, 1, 56), 48, 1, col(48, 456, 56), 48, 456) == C
+    assert gba.shared_layout(col(48, 1, 56), 48, 1, row(48, 456, 464), 48, 456) == R
+    assert gba.operand_layout(col(48, 1, 56), 48, 1, want=C) == (C, 48)
+    # B (1 x 312) is a single row, Q decides
+    assert gba.shared_layout(row(1, 312, 320), 1, 312, col(456, 312, 464), 456, 312) == C
+    assert gba.shared_layout(row(64, 32, 40), 64, 32, row(64, 16, 24), 64, 16) == R
+    with pytest.raises(ValueError):
+        gba.shared_layout(row(64, 32, 40), 64, 32, col(64, 16, 72), 64, 16)

@@ -100,6 +100,16 @@ class Problem:
 
 
 # ----------------------------------------------------------------------------
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_single_column_left_operand_with_a_second_product(layout):
+    """K = 1 makes A a single column (and B a single row), which fits
+    either layout: the binding takes the layout of P (and Q) for it."""
+    announce("K=1 with a second product", layout)
+    pr = Problem(707, 48, 312, 1, K2=456)
+    U.assert_close(pr.gpu(layout, second="add", act="sigmoid"), pr.oracle(second="add", act="sigmoid"),
+                   what=f"K=1 {layout}")
+
+
 def test_earlier_runtime_failure_does_not_fail_a_launch():
     """A failed runtime call made earlier on the same thread (hipSetDevice
     with a device index that does not exist: rejected on the host, nothing
