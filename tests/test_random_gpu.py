@@ -80,6 +80,32 @@ def test_random_request(seed):
     run_case(seed, draw(seed))
 
 
+NUM_CASES_LARGE = 96
+
+
+def draw_large(seed):
+    """A request of 128 to 1024 rows and columns and a reduction of up to
+    1024 (multiples of 8: the aligned fast path), mostly on the library's
+    own tile choice, every other option as in draw()."""
+    c = draw(200000 + seed)
+    rng = np.random.default_rng(555000 + seed)
+    c["M"], c["N"] = int(rng.integers(16, 129)) * 8, int(rng.integers(16, 129)) * 8
+    c["K"], c["K2"] = int(rng.integers(1, 129)) * 8, int(rng.integers(0, 65)) * 8
+    c["offset"] = False
+    c["tile"] = None if rng.random() < 0.8 else int(rng.integers(0, gba.num_tiles()))
+    info = gba.tile_info(c["tile"]) if c["tile"] is not None else None
+    if info and c["accum"] == "f16" and info["split_k"] > 1:
+        c["tile"] = None
+    if c["split"] is not None and info and info["bm"] * info["bn"] > 128 * 128:
+        c["split"] = None
+    return c
+
+
+@pytest.mark.parametrize("seed", range(NUM_CASES_LARGE))
+def test_random_request_large(seed):
+    run_case(300000 + seed, draw_large(seed))
+
+
 @pytest.mark.parametrize("seed", range(NUM_CASES_EIGHT_WAVE))
 def test_random_request_eight_wave_tiles(seed):
     run_case(100000 + seed, draw_eight_wave(seed))
