@@ -403,6 +403,104 @@ def sweep(args, np, torch, D, gba):
     print(json.dumps(summary), flush=True)
 
 
+THIN_SHAPES = ([(M, N, K) for M in (32, 64, 128, 256) for N in (2048, 4096, 8192) for K in (512, 1024, 2048, 4096)] +
+               [(4096, 128, 1024), (8192, 256, 2048), (2048, 64, 4096), (512, 2048, 1024), (1024, 1024, 4096)])
+
+
+SHORTK_SHAPES = [(M, N, K) for (M, N) in ((1024, 2048), (2048, 2048), (2048, 3072), (3072, 2048), (2560, 3072),
+                                           (3072, 3072), (2944, 3200), (3456, 3456), (3840, 3840), (4096, 4096),
+                                           (4096, 2048), (1536, 4096)) for K in (64, 128, 192, 256)]
+
+
+def rule_tile(gba, M, N, K, layout, accum, prologue):
+    """The tile the library chooses for a one-product request of this shape,
+    layout, accumulation and prologue (host-only: gba_fused_tile on a
+    descriptor whose pointers are never dereferenced)."""
+    la = gba.GBA_ROW_MAJOR if layout[0] == "R" else gba.GBA_COL_MAJOR
+    lb = gba.GBA_ROW_MAJOR if layout[1] == "R" else gba.GBA_COL_MAJOR
+    d = gba.new_desc()
+    d.layoutA, d.layoutB, d.M, d.N, d.K = la, lb, M, N, K
+    d.A = d.B = d.C = d.bias = 1 << 16
+    d.lda = K if la == gba.GBA_ROW_MAJOR else M
+    d.ldb = N if lb == gba.GBA_ROW_MAJOR else K
+    d.ldc, d.bias_kind, d.act = N, gba.GBA_BIAS_ROW, gba.GBA_ACT_RELU
+    d.prologue = gba.GBA_PRO_RELU if prologue else gba.GBA_PRO_NONE
+    d.accum = gba.GBA_ACC_F16 if accum == "f16" else gba.GBA_ACC_F32
+    return gba.fused_tile(d)
+
+
+def tile_sweep(args, np, torch, D, gba):
+    """Every tile against the library's choice: for each shape of a set (the
+    thin set, or the workload shapes plus 40 random multiples of 128 for a
+    seed), every tile that fits is graph-timed warm (the same operands each
+    launch) and with operands from HBM (launches rotate over copies of the
+    operands spanning at least 1 GiB).  One JSON line per shape, then a
+    summary: the library's choice against the per-shape best tile, in total
+    time over the set."""
+    if args.tile_sweep == "thin":
+        shapes = THIN_SHAPES
+    elif args.tile_sweep == "shortk":
+        shapes = SHORTK_SHAPES
+    else:
+        shapes = ([(4096, 4096, 4096), (8192, 4096, 1024), (8192, 1024, 4096), (1024, 1024, 1024),
+                   (1000, 1000, 1000), (32, 4096, 1024), (128, 4096, 1024), (256, 4096, 1024),
+                   (2048, 2048, 2048), (64, 512, 32768), (512, 512, 8192)] +
+                  D.sweep_shapes(int(args.tile_sweep), 40))
+    lay, acc, pro = args.layout, args.accum, args.prologue
+    operand = lambda x, colmajor: x.t().contiguous().t() if colmajor else x
+
+    def graph(fn, n):
+        fn(0)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(n):
+                fn(i)
+        g.replay()
+        torch.cuda.synchronize()
+        return g, n
+
+    def run(g, n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n * 1000
+
+    tot = {"rule": [0.0, 0.0], "best": [0.0, 0.0]}
+    for idx, (M, N, K) in enumerate(shapes):
+        nc = max(2, min(64, (1 << 30) // ((M * K + N * K) * 2) + 1))
+        gen = torch.Generator(device="cuda").manual_seed(770000 + idx)
+        As = [operand(torch.rand(M, K, generator=gen, device="cuda").half() - 0.5, lay[0] == "C") for _ in range(nc)]
+        Bs = [operand(torch.rand(K, N, generator=gen, device="cuda").half() - 0.5, lay[1] == "C") for _ in range(nc)]
+        bias = torch.rand(N, generator=gen, device="cuda").half()
+        out = torch.empty(M, N, dtype=torch.float16, device="cuda")
+        kw = dict(bias=bias, out=out, accum=acc, prologue="relu" if pro else None, workspace=None)
+        warm, cold = {}, {}
+        for t in range(gba.num_tiles()):
+            info = gba.tile_info(t)
+            if info["bm"] > M or info["bn"] > N or (acc == "f16" and info["split_k"] > 1):
+                continue
+            gw = graph(lambda i, t=t: gba.fused_gemm(As[0], Bs[0], tile=t, **kw), 10)
+            gc = graph(lambda i, t=t: gba.fused_gemm(As[i % nc], Bs[i % nc], tile=t, **kw), max(10, nc))
+            warm[t] = round(min(run(*gw) for _ in range(5)), 2)
+            cold[t] = round(min(run(*gc) for _ in range(3)), 2)
+        rule = rule_tile(gba, M, N, K, lay, acc, pro)
+        print(json.dumps({"M": M, "N": N, "K": K, "rule": rule, "warm": warm, "cold": cold}), flush=True)
+        if rule in warm:
+            tot["rule"][0] += warm[rule]
+            tot["rule"][1] += cold[rule]
+            tot["best"][0] += min(warm.values())
+            tot["best"][1] += min(cold.values())
+        del As, Bs, out
+        torch.cuda.empty_cache()
+    print(json.dumps({"tile_sweep": args.tile_sweep, "layout": lay, "accum": acc, "prologue": pro,
+                      "shapes": len(shapes),
+                      "rule_over_best_warm": round(tot["rule"][0] / tot["best"][0], 4),
+                      "rule_over_best_cold": round(tot["rule"][1] / tot["best"][1], 4)}), flush=True)
+
+
 def ksweep(args, np, torch, D, gba):
     """Fixed cost and cost per reduction step of the fused kernel: at fixed
     M x N (the two MLP shapes, 1024^2 and 4096^2, RC, fp32 accumulation,
@@ -480,6 +578,13 @@ def main():
     ap.add_argument("--sweep", type=int, nargs="?", const=100, default=0, metavar="N",
                     help="instead of the headline line: the paper's protocol over N random "
                          "sizes (default 100), one line per size and a summary line")
+    ap.add_argument("--tile-sweep", default=None, metavar="SET",
+                    help="instead of the headline line: every tile against the library's choice "
+                         "over a shape set ('thin', 'shortk', or a seed for the workload shapes "
+                         "plus 40 random ones), warm and with operands from HBM")
+    ap.add_argument("--layout", default="RC", choices=["RR", "RC", "CR", "CC"], help="with --tile-sweep")
+    ap.add_argument("--accum", default="f32", choices=["f32", "f16"], help="with --tile-sweep")
+    ap.add_argument("--prologue", action="store_true", help="with --tile-sweep: ReLU prologue on A")
     args = ap.parse_args()
 
     if args.calibrate_copy:
@@ -513,6 +618,9 @@ def main():
         return
     if args.ksweep:
         ksweep(args, np, torch, D, gba)
+        return
+    if args.tile_sweep:
+        tile_sweep(args, np, torch, D, gba)
         return
     w = D.WORKLOADS[args.workload]
     A, B, bias = D.logical_inputs(w)

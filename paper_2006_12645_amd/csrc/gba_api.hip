@@ -124,6 +124,31 @@ int select_tile(int64_t M, int64_t N, int64_t K, int accum, int la, int lb, bool
         return tile_fits(t, M, N) ? ceil_div(M, TILES[t].bm) * ceil_div(N, TILES[t].bn) : 0;
     };
     const double ai = (double)M * N * K / ((double)M * K + (double)K * N + (double)M * N + 1.0);
+    // Short reductions (K <= 256) over 1024 or more rows and columns: two to
+    // four 64-deep steps, where a large tile's pipeline fill and epilogue
+    // outweigh its steps.  With column-major B (either accumulation): 256x256
+    // from 208 workgroups, else 128x128 from 256, else the 8-wave tile with
+    // its long side along the longer output side; with row-major B (fp32):
+    // 256x256 from 256 workgroups, else the 4-wave 128x128 tile from 384,
+    // else the 4-wave 128x64 / 64x128 one.  On 48 shapes (1024-4096 rows and
+    // columns, K = 64-256) per layout, warm / with operands from HBM: RC
+    // 1.9% / 1.8% and CC 1.7% / 1.5% over the per-shape best tile (fp32; fp16
+    // 3.3% / 2.8% and 2.6% / 2.0%), RR 3.1% / 3.3% and CR 2.7% / 2.8%,
+    // against 4.4% / 3.7%, 3.9% / 3.5% (fp16 4.2% / 3.4%, 3.3% / 2.5%), 15% /
+    // 13% and 11% / 10% for the rule below (3072x3072x128 RR: 12.1 / 11.9 us
+    // on 128x64 against 16.6 / 16.4 on 256x256).
+    if (K <= 256 && M >= 1024 && N >= 1024) {
+        if (lb == GBA_COL_MAJOR) {
+            if (tiles(1) >= 208) return 1;
+            if (tiles(18) >= 256) return 18;
+            return N > M ? 20 : 19;
+        }
+        if (accum == GBA_ACC_F32) {
+            if (tiles(1) >= 256) return 1;
+            if (tiles(4) >= 384) return 4;
+            return N > M ? 7 : 5;
+        }
+    }
     if (accum == GBA_ACC_F16) {
         // fp16 accumulation: the 256x256 tile (which then keeps every wave
         // issuing copies) only from 208 workgroups; below

@@ -110,6 +110,14 @@ def test_cr_never_takes_four_stage_small_tiles(accum, prologue):
     # k-groups 7.58 / 9.07 against 7.38 / 10.58 on the four-stage 32x32 tile
     (dict(M=64, N=4096, K=2048), 13),
     (dict(M=64, N=4096, K=1024), 23),
+    # short reductions: RR 3072 x 3072 x 128 on the 4-wave 128x128 tile
+    # 13.1 / 12.8 against 16.8 / 16.4 on 256x256 (128x64: 12.1 / 11.9; the
+    # branch's 384-workgroup limit for 128x128 was the best single limit
+    # over the 48 shapes); RC 3200 x 2944 x 128 on the 8-wave 128x128 tile
+    # 11.9 / 11.3 against 12.5 / 12.3; 4096^2 x 128 stays on 256x256
+    (dict(M=3072, N=3072, K=128, layout="RR"), 4),
+    (dict(M=3200, N=2944, K=128), 18),
+    (dict(M=4096, N=4096, K=128), 1),
     # a requested tile that fits is kept
     (dict(M=1024, N=1024, K=1024, layout="RR", prologue=True, tile=24), 24),
 ])
