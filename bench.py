@@ -414,19 +414,10 @@ SHORTK_SHAPES = [(M, N, K) for (M, N) in ((1024, 2048), (2048, 2048), (2048, 307
 
 def rule_tile(gba, M, N, K, layout, accum, prologue):
     """The tile the library chooses for a one-product request of this shape,
-    layout, accumulation and prologue (host-only: gba_fused_tile on a
-    descriptor whose pointers are never dereferenced)."""
+    layout, accumulation and prologue (host-only)."""
     la = gba.GBA_ROW_MAJOR if layout[0] == "R" else gba.GBA_COL_MAJOR
     lb = gba.GBA_ROW_MAJOR if layout[1] == "R" else gba.GBA_COL_MAJOR
-    d = gba.new_desc()
-    d.layoutA, d.layoutB, d.M, d.N, d.K = la, lb, M, N, K
-    d.A = d.B = d.C = d.bias = 1 << 16
-    d.lda = K if la == gba.GBA_ROW_MAJOR else M
-    d.ldb = N if lb == gba.GBA_ROW_MAJOR else K
-    d.ldc, d.bias_kind, d.act = N, gba.GBA_BIAS_ROW, gba.GBA_ACT_RELU
-    d.prologue = gba.GBA_PRO_RELU if prologue else gba.GBA_PRO_NONE
-    d.accum = gba.GBA_ACC_F16 if accum == "f16" else gba.GBA_ACC_F32
-    return gba.fused_tile(d)
+    return gba.select_tile(M, N, K, la, lb, accum=accum, prologue=prologue)
 
 
 def tile_sweep(args, np, torch, D, gba):

@@ -426,8 +426,20 @@ def tile_info(tile_id):
     return dict(zip(("bm", "bn", "bk", "waves", "split_k"), (v.value for v in vals)))
 
 
-def select_tile(M, N, K, layout_a=GBA_ROW_MAJOR, layout_b=GBA_COL_MAJOR, accum="f32"):
-    return lib().gba_select_tile(layout_a, layout_b, M, N, K, ACCS[accum])
+def select_tile(M, N, K, layout_a=GBA_ROW_MAJOR, layout_b=GBA_COL_MAJOR, accum="f32", prologue=False):
+    """Tile id the library would run a one-product request of this shape
+    on (K: the total reduction length), -1 for the general path.  With the
+    prologue the choice can differ; it is then asked through
+    gba_fused_tile on a descriptor whose pointers are never dereferenced."""
+    if not prologue:
+        return lib().gba_select_tile(layout_a, layout_b, M, N, K, ACCS[accum])
+    d = new_desc()
+    d.layoutA, d.layoutB, d.M, d.N, d.K = layout_a, layout_b, M, N, K
+    d.A = d.B = d.C = 1 << 16
+    d.lda = K if layout_a == GBA_ROW_MAJOR else M
+    d.ldb = N if layout_b == GBA_ROW_MAJOR else K
+    d.ldc, d.act, d.accum, d.prologue = N, GBA_ACT_RELU, ACCS[accum], GBA_PRO_RELU
+    return fused_tile(d)
 
 
 def version():

@@ -125,6 +125,16 @@ def test_measured_choices(case, tile):
     assert gba.fused_tile(desc(**case)) == tile
 
 
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("accum", ACCS)
+def test_select_tile_with_prologue_is_fused_tile(layout, accum):
+    la, lb = LAYOUTS[layout]
+    for M, N, K in shapes(14, 200):
+        for pro in (False, True):
+            want = gba.fused_tile(desc(M, N, K, layout, accum, prologue=pro))
+            assert gba.select_tile(M, N, K, la, lb, accum=accum, prologue=pro) == want, (M, N, K, pro)
+
+
 def test_fused_tile_errors():
     t = ctypes.c_int(5)
     assert gba.lib().gba_fused_tile(ctypes.byref(desc(64, 64, 64)), None) == gba.GBA_EINVAL
